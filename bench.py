@@ -1,0 +1,263 @@
+#!/usr/bin/env python3
+"""Bench of the GliDe + CaPE decoding hot path on one MI355X.
+
+One step = one pass of the whole hot path over one batch of synthetic input,
+in the order a decoding round runs it:
+  1. cape_expand        draft distributions -> expanded proposal tree;
+  2. glide_tree_attn    one verification attention launch per target layer,
+                        with the tree just built (tree mode);
+  3. glide_argmax_rows  the target's greedy token per tree row;
+  4. tree_verify        accept length, last node and bonus token;
+  5. glide_tree_attn    the GliDe cross-attention of the draft's gamma query
+                        rows into the top target layer's cache (cross mode),
+                        for workloads that have one.
+Inputs are generated and resident in HBM before timing starts.
+
+Default workload: Vicuna-7B verify step (32 layers x 32 heads, head_dim 128,
+batch 1, prefix 2048, 16-node CaPE tree of depth 5 with top-k 3) plus one
+5-query GliDe cross-attention layer.
+
+Prints one JSON line.  `value` is the attention bytes per step (K/V rows read,
+Q read, O written; the algorithmic count, split partials excluded) divided by
+the wall time of the whole step.
+"""
+
+import argparse
+import json
+import os
+import sys
+import time
+
+import numpy as np
+import torch
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+if ROOT not in sys.path:
+    sys.path.insert(0, ROOT)
+
+import paper_2402_02082_amd as glide  # noqa: E402
+from synth import workloads as W  # noqa: E402
+
+HBM_PEAK_GBPS = 8000.0
+METRIC = "tree-attn KV-read GB/s (% of HBM peak); µs per verify step at 7B shape"
+SEED = 2
+
+
+def attn_bytes(lens, n_q, heads, elem, tree):
+    """Algorithmic HBM bytes of one attention launch: every visible K/V row
+    once, the query rows once, the output rows once."""
+    keys = sum(int(l) + (n_q if tree else 0) for l in lens)
+    return heads * (2 * keys * 128 * elem + 2 * len(lens) * n_q * 128 * elem)
+
+
+class Step:
+    """Device-resident inputs and outputs of one workload, and its step."""
+
+    def __init__(self, wl, dtype, seed, max_splits=0):
+        dev = torch.device("cuda")
+        self.wl, self.dev, self.max_splits = wl, dev, max_splits
+        B, N, V = wl.batch, wl.nodes, wl.vocab
+        self.lens_np = W.prefix_lengths(wl, seed)
+        self.lens = torch.from_numpy(self.lens_np).to(dev)
+        if wl.tree == "cape":
+            probs, chain, leaf = W.draft_probs(wl, seed)
+            logits, self.planted, _ = W.planted_logits_cape(wl, seed, chain, leaf, probs)
+            self.probs_np = probs
+            self.probs = torch.from_numpy(probs).to(dev)
+        else:
+            cand = W.chain_tokens(wl, seed)
+            logits, self.planted = W.planted_logits_chain(wl, seed, cand)
+            self.probs = None
+            self.chain_tokens = torch.from_numpy(cand).to(dev)
+            self.chain_parents = torch.from_numpy(
+                np.tile(np.arange(-1, N - 1, dtype=np.int32), (B, 1))).to(dev)
+        self.logits_np = logits
+        self.logits = torch.from_numpy(logits).to(dev)
+        self.layers = [W.attention_layer(wl, seed, l, dtype, dev) for l in range(wl.layers)]
+        self.outs = [torch.empty_like(q) for q, _, _ in self.layers]
+        self.cross_q = W.cross_queries(wl, seed, dtype, dev) if wl.cross else None
+        self.cross_out = torch.empty_like(self.cross_q) if wl.cross else None
+        self.tokens = torch.empty((B, N), dtype=torch.int32, device=dev)
+        self.parents = torch.empty((B, N), dtype=torch.int32, device=dev)
+        self.n_nodes = torch.empty((B,), dtype=torch.int32, device=dev)
+        self.ta = torch.empty((B, N + 1), dtype=torch.int32, device=dev)
+        self.acc = torch.empty((B,), dtype=torch.int32, device=dev)
+        self.last = torch.empty((B,), dtype=torch.int32, device=dev)
+        self.bonus = torch.empty((B,), dtype=torch.int32, device=dev)
+        L_cap = wl.l_cap
+        self.ws = glide.attn_workspace(B, N, wl.heads, L_cap, max_splits, dev)
+        self.xws = (glide.attn_workspace(B, wl.depth, wl.heads, L_cap, max_splits, dev)
+                    if wl.cross else None)
+        elem = 2 if dtype == torch.bfloat16 else 4
+        self.verify_bytes = attn_bytes(self.lens_np, N, wl.heads, elem, True)
+        self.cross_bytes = attn_bytes(self.lens_np, wl.depth, wl.heads, elem, False) \
+            if wl.cross else 0
+
+    def run(self, attn_events=None):
+        wl = self.wl
+        if self.probs is not None:
+            glide.cape_expand(self.probs, wl.k, wl.nodes, self.tokens, self.parents, self.n_nodes)
+            tokens, parents = self.tokens, self.parents
+        else:
+            tokens, parents = self.chain_tokens, self.chain_parents
+        for i, ((q, k, v), o) in enumerate(zip(self.layers, self.outs)):
+            if attn_events is not None:
+                attn_events[i][0].record()
+            glide.glide_tree_attn(q, k, v, self.lens, parents, o, max_splits=self.max_splits,
+                                  workspace=self.ws)
+            if attn_events is not None:
+                attn_events[i][1].record()
+        glide.glide_argmax_rows(self.logits, self.ta)
+        glide.tree_verify(self.ta, tokens, parents, self.acc, self.last, self.bonus)
+        if wl.cross:
+            _, k, v = self.layers[-1]
+            glide.glide_tree_attn(self.cross_q, k, v, self.lens, None, self.cross_out,
+                                  max_splits=self.max_splits, workspace=self.xws)
+
+
+def cpu_baseline(step, budget_s=12.0):
+    """The float64 oracle on a bounded sample of the same step: the CaPE
+    expansion, argmax and verification in full, then verification-attention
+    layers (all heads) until ~budget_s, then the cross-attention layer.
+    Reported in the metric's unit (attention GB/s) with the BLAS threads used."""
+    import threadpoolctl
+
+    from oracle import attention as OA
+    from oracle import cape as OC
+    from oracle import verify as OV
+
+    wl = step.wl
+    f64 = lambda t: t.float().cpu().numpy().astype(np.float64)  # noqa: E731
+    with threadpoolctl.threadpool_limits(1):
+        t0 = time.perf_counter()
+        if wl.tree == "cape":
+            tokens, parents, _ = OC.cape_expand(step.probs_np, wl.k, wl.nodes)
+        else:
+            tokens = step.chain_tokens.cpu().numpy()
+            parents = step.chain_parents.cpu().numpy()
+        ta = OV.argmax_rows(step.logits_np)
+        OV.tree_verify(ta, tokens, parents)
+        t_int = time.perf_counter() - t0
+        t_attn, nbytes, layers_done = 0.0, 0, 0
+        for (q, k, v) in step.layers:
+            qh, kh, vh = f64(q), f64(k), f64(v)
+            t1 = time.perf_counter()
+            OA.tree_attention(qh, kh, vh, step.lens_np, parents)
+            t_attn += time.perf_counter() - t1
+            nbytes += step.verify_bytes
+            layers_done += 1
+            if t_attn + t_int > budget_s:
+                break
+        if wl.cross:
+            _, k, v = step.layers[-1]
+            t1 = time.perf_counter()
+            OA.tree_attention(f64(step.cross_q), f64(k), f64(v), step.lens_np, None)
+            t_attn += time.perf_counter() - t1
+            nbytes += step.cross_bytes
+    total = t_attn + t_int
+    return {"value": round(nbytes / total / 1e9, 6), "unit": "GB/s", "cores": 1, "kind": "oracle",
+            "sample": "%s: CaPE expansion, argmax and tree verification in full, %d of %d "
+                      "verification-attention layers (all heads)%s, float64 NumPy, %.1f s"
+                      % (wl.name, layers_done, wl.layers, " + the cross-attention layer"
+                         if wl.cross else "", total)}
+
+
+def load_traffic():
+    """HBM bytes per tree-attention launch from the committed rocprofv3 PMC
+    summary, if one matches the current kernel build (else None)."""
+    path = os.path.join(ROOT, "profiles", "tree_attn_vicuna7b_pmc.json")
+    if not os.path.exists(path):
+        return None
+    try:
+        rec = json.load(open(path))
+        return rec.get("traffic_bytes_per_launch")
+    except (OSError, ValueError):
+        return None
+
+
+def main():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=30)
+    ap.add_argument("--warmup", type=int, default=5)
+    ap.add_argument("--workload", type=int, default=2, choices=sorted(W.WORKLOADS))
+    ap.add_argument("--max-splits", type=int, default=0)
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    args = ap.parse_args()
+    if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
+        print("bench.py measures one GPU only: the hot path here is a single-GPU kernel set and "
+              "no multi-GPU figure is produced (run with --gpus 1)", file=sys.stderr)
+        sys.exit(2)
+    if not torch.cuda.is_available():
+        print("bench.py needs a GPU", file=sys.stderr)
+        sys.exit(2)
+    glide.load()
+
+    wl = W.WORKLOADS[args.workload]
+    dtype = torch.bfloat16
+    step = Step(wl, dtype, SEED, args.max_splits)
+    torch.cuda.synchronize()
+
+    for _ in range(args.warmup):
+        step.run()
+    torch.cuda.synchronize()
+
+    # Timed region: K whole steps, per-launch events on the attention kernels.
+    ev = [[(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True))
+           for _ in range(wl.layers)] for _ in range(args.steps)]
+    start, stop = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    torch.cuda.synchronize()
+    start.record()
+    for i in range(args.steps):
+        step.run(ev[i])
+    stop.record()
+    torch.cuda.synchronize()
+    ms_step = start.elapsed_time(stop) / args.steps
+    per_launch = [a.elapsed_time(b) for e in ev for a, b in e]
+    launch_ms = float(np.mean(per_launch))
+    verify_us = float(np.mean([ev[i][0][0].elapsed_time(ev[i][-1][1])
+                               for i in range(args.steps)])) * 1e3
+
+    # Untimed check that the last step produced the planted acceptance.
+    acc = step.acc.cpu().numpy()
+    planted_ok = bool(np.array_equal(acc, step.planted))
+
+    step_bytes = step.verify_bytes + step.cross_bytes
+    value = step_bytes / (ms_step * 1e-3) / 1e9
+    per_launch_bytes = step.verify_bytes / wl.layers
+    achieved = per_launch_bytes / (launch_ms * 1e-3) / 1e9
+    rec = {
+        "metric": METRIC,
+        "value": round(value, 3),
+        "unit": "GB/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": round(ms_step, 4),
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "bf16",
+        "data": "synthetic",
+        "config": {"workload": wl.name, "layers": wl.layers, "heads": wl.heads,
+                   "head_dim": wl.head_dim, "batch": wl.batch,
+                   "prefix": [int(x) for x in step.lens_np], "tree_nodes": wl.nodes,
+                   "tree_depth": wl.depth, "top_k": wl.k, "vocab": wl.vocab,
+                   "cross_attn_queries": wl.depth if wl.cross else 0, "seed": SEED},
+        "us_per_verify_step": round(verify_us, 2),
+        "hbm_frac_of_step": round(value / HBM_PEAK_GBPS, 4),
+        "planted_accept_len_ok": planted_ok,
+        "roofline": {"bound": "hbm", "achieved": round(achieved, 2), "peak": HBM_PEAK_GBPS,
+                     "unit": "GB/s", "frac": round(achieved / HBM_PEAK_GBPS, 4),
+                     "traffic": load_traffic(),
+                     "kernel": "tree_attn_kernel (verification, per layer)",
+                     "bytes_per_launch": per_launch_bytes,
+                     "avg_launch_us": round(launch_ms * 1e3, 3)},
+    }
+    if not args.no_cpu_baseline:
+        rec["cpu_baseline"] = cpu_baseline(step)
+    print(json.dumps(rec), flush=True)
+
+
+if __name__ == "__main__":
+    main()

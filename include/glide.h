@@ -1,0 +1,183 @@
+/*
+ * glide.h -- C ABI of the GliDe + CaPE decoding hot path for MI355X (gfx950).
+ *
+ * Operations (arXiv 2402.02082, "GliDe with a CaPE"):
+ *   glide_tree_attn    softmax attention of a few query rows against a long
+ *                      KV cache, either under the CaPE tree mask (target
+ *                      verification, Sec. 4.2 "Verification of Expanded
+ *                      Proposals", mask_CaPE equation) or unmasked (GliDe
+ *                      cross-attention into the target cache, Sec. 4.1,
+ *                      MultiHead / hd_j equations).
+ *   cape_expand        confidence-aware proposal expansion and linearisation
+ *                      into a parent-indexed tree (Sec. 4.2 "Proposal
+ *                      Expansion", S(p) table).
+ *   glide_argmax_rows  the target's greedy token per logits row (Sec. 3,
+ *                      greedy "speculative decoding" acceptance).
+ *   tree_verify        greedy longest-accepted-path selection (Sec. 3;
+ *                      Sec. 5.1 "Experiment design": greedy acceptance for
+ *                      the CaPE experiments).
+ *
+ * Conventions shared by every call:
+ *   - All array arguments are DEVICE pointers to memory the caller owns and
+ *     allocated; the library never allocates or frees memory on these paths
+ *     and never keeps a pointer after the call returns.
+ *   - Work is enqueued on `stream` (NULL = the default stream) and the call
+ *     returns without synchronising.  Outputs are valid once the stream
+ *     reaches that point.
+ *   - Every scalar/pointer argument is checked on the host BEFORE any HIP
+ *     call; a bad argument returns GLIDE_EINVAL and touches nothing.  Device
+ *     data (sequence lengths, parent arrays) is trusted unless the environment
+ *     variable GLIDE_VALIDATE=1 is set, in which case it is copied to the host
+ *     (synchronising the stream) and checked, returning GLIDE_ERANGE when out
+ *     of range.  Unvalidated out-of-range data never causes an out-of-bounds
+ *     access: lengths are clamped and bad parents are treated as roots.
+ *   - A failed kernel launch returns GLIDE_EHIP; glide_last_hip_error() gives
+ *     the HIP error code of the calling thread's last failure.
+ *   - int32 tree arrays: node index = position in the linearised proposal;
+ *     parents[n] in [-1, n) (-1 = child of the accepted prefix).
+ */
+#ifndef GLIDE_H
+#define GLIDE_H
+
+#include <stddef.h>
+#include <stdint.h>
+#include <hip/hip_runtime_api.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+/* Status codes. */
+#define GLIDE_OK      0
+#define GLIDE_EINVAL  1   /* bad pointer, size, dtype or option */
+#define GLIDE_ERANGE  2   /* device data out of range (GLIDE_VALIDATE=1 only) */
+#define GLIDE_EHIP    3   /* a HIP call or kernel launch failed */
+
+/* Element types of q / k_cache / v_cache / out. */
+#define GLIDE_BF16    0   /* bfloat16 in and out, float32 accumulation */
+#define GLIDE_F32     1   /* float32 in and out, float32 accumulation */
+
+#define GLIDE_MAX_NODES   64   /* tree nodes / query rows per sequence */
+#define GLIDE_MAX_SPLITS  64   /* key-range splits per (sequence, head) */
+#define GLIDE_HEAD_DIM    128  /* the only head dimension supported */
+#define GLIDE_CAPE_MAX_K  7    /* largest expansion set, max of S(p) */
+
+/* Human-readable name of a status code (static storage, never NULL). */
+const char* glide_strerror(int status);
+
+/* HIP error code (hipError_t as int) of the calling thread's last
+ * GLIDE_EHIP, or 0. */
+int glide_last_hip_error(void);
+
+/*
+ * Workspace bytes glide_tree_attn needs for these sizes (0 when the call runs
+ * without a workspace, i.e. with one split).  Arguments as glide_tree_attn.
+ * The workspace holds per-split partial softmax states and one completion
+ * counter per (sequence, head).  It must be zero-filled ONCE after allocation
+ * (every call leaves the counters at zero again) and must not be shared by
+ * calls that can run concurrently.  Returns 0 for invalid sizes as well.
+ */
+size_t glide_tree_attn_workspace(int B, int N, int H, int D, int L_cap,
+                                 int max_splits);
+
+/*
+ * glide_tree_attn -- one attention layer of the verification pass (tree mode)
+ * or the GliDe cross-attention (cross mode).
+ *
+ * Sec. 4.1: hd_j = SoftMax(Q K^T / sqrt(d_k)) V per head j.
+ * Tree mode (tree_parents != NULL): query row n of sequence b sees cache rows
+ *   [0, seq_lens[b]) (the accepted prefix) and the rows seq_lens[b] + m of
+ *   every tree node m that is node n or one of its ancestors -- the
+ *   ancestor-or-self relation that mask_CaPE (Sec. 4.2) defines for a
+ *   linearised expanded proposal.  The caller has written the tree nodes'
+ *   keys/values at cache rows [seq_lens[b], seq_lens[b] + N).
+ * Cross mode (tree_parents == NULL): every query row sees rows
+ *   [0, seq_lens[b]) and nothing else (Sec. 4.1: the draft's queries attend
+ *   the target cache up to position t-1; no mask at inference).
+ *
+ *   q            [B, N, H, D]  dtype; query rows (post-RoPE, unscaled).
+ *   k_cache      [B, H, L_cap, D] dtype, contiguous.
+ *   v_cache      [B, H, L_cap, D] dtype, contiguous.
+ *   seq_lens     [B] int32: prefix length L_b.  Clamped to [0, L_cap - N]
+ *                (tree) or [0, L_cap] (cross).
+ *   tree_parents [B, N] int32 or NULL (cross mode).
+ *   out          [B, N, H, D]  dtype; may not alias the inputs.  Rows of a
+ *                sequence with no visible key (cross mode, L_b = 0) are 0.
+ *   B >= 1; 1 <= N <= 64; H >= 1; D == 128; L_cap >= N (tree) or >= 1.
+ *   dtype        GLIDE_BF16 or GLIDE_F32.
+ *   scale        softmax scale; <= 0 selects 1/sqrt(D).
+ *   max_splits   0 = choose automatically, else 1..64 key-range splits.
+ *   workspace    device buffer of >= glide_tree_attn_workspace(...) bytes,
+ *                zero-filled once; may be NULL when that size is 0.
+ */
+int glide_tree_attn(const void* q, const void* k_cache, const void* v_cache,
+                    const int32_t* seq_lens, const int32_t* tree_parents,
+                    void* out, int B, int N, int H, int D, int L_cap,
+                    int dtype, float scale, int max_splits,
+                    void* workspace, size_t ws_bytes, hipStream_t stream);
+
+/* Workspace bytes cape_expand needs (the per-row top candidates). */
+size_t cape_expand_workspace(int B, int gamma);
+
+/*
+ * cape_expand -- confidence-aware proposal expansion (Sec. 4.2).
+ *
+ * For each sequence b and position i < gamma, with row p = draft_probs[b, i]:
+ *   x_i = the most probable token (ties: lower id), p_i = its probability;
+ *   K_i = S(p_i) = 7, 5, 3, 1 for p_i in (0,0.3], (0.3,0.6], (0.6,0.8],
+ *         (0.8,1] (float32 edges, upper bounds inclusive), capped by k when
+ *         k > 0; with fixed != 0, K_i = k for every i (the fixed-size
+ *         ablation, Sec. 5.4); always K_i <= V - 1;
+ *   X_i = the K_i most probable tokens other than x_i (ties: lower id).
+ * Tree: node i < gamma is x_i with parent i - 1; the leaves of X_0, X_1, ...
+ * follow in position order, rank order within a position, each with the
+ * parent of its position's proposal token.  If gamma + sum K_i > n_max (the
+ * verification budget, Sec. 5.3), the n_max - gamma leaves kept are the first
+ * in the order (prob desc, position asc, rank asc).  Unused slots are
+ * (token -1, parent -1).
+ *
+ *   draft_probs [B, gamma, V] float32, finite (no NaN).
+ *   tokens_out, parents_out [B, n_max] int32; n_nodes_out [B] int32.
+ *   B >= 1; 1 <= gamma <= n_max <= 64; V >= 2; 0 <= k (<= 7 when fixed).
+ *   workspace >= cape_expand_workspace(B, gamma) bytes (no zero-fill needed).
+ */
+int cape_expand(const float* draft_probs, int B, int gamma, int V, int k,
+                int fixed, int n_max, int32_t* tokens_out,
+                int32_t* parents_out, int32_t* n_nodes_out,
+                void* workspace, size_t ws_bytes, hipStream_t stream);
+
+/*
+ * glide_argmax_rows -- idx_out[r] = argmax_v logits[r, v], ties to the lower
+ * index (Sec. 3: greedy acceptance compares against the target's greedy
+ * token).  -0.0 and +0.0 compare equal; NaN is not allowed.
+ *   logits [rows, V] float32 row-major; idx_out [rows] int32.
+ *   rows >= 1; V >= 1.
+ */
+int glide_argmax_rows(const float* logits, int rows, int V, int32_t* idx_out,
+                      hipStream_t stream);
+
+/*
+ * tree_verify -- greedy acceptance of a candidate tree (Sec. 3, Sec. 4.2).
+ *
+ * Node c is accepted when its parent is accepted (or c is a root) and
+ * cand_tokens[c] == target_argmax[parents[c] + 1].  accept_len = the depth
+ * of the deepest accepted node (0 if none); last_node = that node (lowest
+ * index among equals; -1 if none); bonus = target_argmax[last_node + 1], the
+ * free token the target contributes.
+ *
+ *   target_argmax [B, N + 1] int32: slot 0 = the target's greedy token after
+ *                 the prefix, slot n + 1 = after tree node n.
+ *   cand_tokens   [B, N] int32 (padding nodes carry -1 and never match).
+ *   parents       [B, N] int32.
+ *   accept_len    [B] int32 out;  last_node, bonus [B] int32 out, nullable.
+ *   B >= 1; 1 <= N <= 64.
+ */
+int tree_verify(const int32_t* target_argmax, const int32_t* cand_tokens,
+                const int32_t* parents, int B, int N, int32_t* accept_len,
+                int32_t* last_node, int32_t* bonus, hipStream_t stream);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* GLIDE_H */

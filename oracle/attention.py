@@ -58,7 +58,7 @@ def attention_rows(q_rows, k_rows, v_rows, scale):
     return p @ v_rows
 
 
-def tree_attention_head(q_h, k_h, v_h, seq_len, parents_b=None, scale=None):
+def tree_attention_head(q_h, k_h, v_h, seq_len, parents_b=None, scale=None, nodes=None):
     """One (sequence, head) unit of the hot path.
 
     q_h [N, D]: the N query rows of this head.
@@ -66,6 +66,7 @@ def tree_attention_head(q_h, k_h, v_h, seq_len, parents_b=None, scale=None):
     seq_len: accepted prefix length L_b.
     parents_b [N] or None: tree parents (verification role) or None (GliDe
     cross-attention role: every query sees rows [0, L_b) and nothing else).
+    nodes: optional subset of query rows to evaluate (the others stay 0).
     Returns [N, D] float64.
     """
     q_h = np.asarray(q_h, dtype=np.float64)
@@ -76,7 +77,7 @@ def tree_attention_head(q_h, k_h, v_h, seq_len, parents_b=None, scale=None):
         scale = 1.0 / np.sqrt(d)
     L = int(seq_len)
     out = np.zeros((n_q, d), dtype=np.float64)
-    for n in range(n_q):
+    for n in (range(n_q) if nodes is None else nodes):
         if parents_b is None:
             rows = list(range(L))
         else:

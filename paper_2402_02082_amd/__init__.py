@@ -1,0 +1,18 @@
+"""GliDe + CaPE decoding hot path for MI355X (gfx950).
+
+Thin Python face of libglide.so (HIP kernels behind a C ABI, declared in
+include/glide.h).  Functions carry the C names:
+
+    glide_tree_attn   tree-masked / cross attention against a KV cache
+    cape_expand       confidence-aware proposal expansion into a tree
+    glide_argmax_rows the target's greedy token per logits row
+    tree_verify       greedy longest-accepted-path selection
+
+PyTorch only provides device memory and streams.
+"""
+
+from ._lib import (  # noqa: F401
+    CAPE_MAX_K, GLIDE_BF16, GLIDE_EHIP, GLIDE_EINVAL, GLIDE_ERANGE, GLIDE_F32, GLIDE_OK,
+    HEAD_DIM, MAX_NODES, MAX_SPLITS, GlideError, attn_workspace, cape_expand,
+    glide_argmax_rows, glide_tree_attn, load, tree_verify,
+)

@@ -1,0 +1,196 @@
+"""ctypes binding of libglide.so: argument marshalling only.
+
+Every function here checks shapes/dtypes/devices of the torch tensors it is
+given, takes their device pointers and calls the C entry point of the same
+name.  No computation happens in Python and there is no fallback: if the
+library is missing or a call fails, an exception is raised.
+"""
+
+import ctypes
+import os
+
+import torch
+
+_PKG = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(_PKG, "libglide.so")
+
+GLIDE_OK, GLIDE_EINVAL, GLIDE_ERANGE, GLIDE_EHIP = 0, 1, 2, 3
+GLIDE_BF16, GLIDE_F32 = 0, 1
+MAX_NODES, MAX_SPLITS, HEAD_DIM, CAPE_MAX_K = 64, 64, 128, 7
+
+_lib = None
+
+
+class GlideError(RuntimeError):
+    def __init__(self, fn, status):
+        lib = load()
+        msg = lib.glide_strerror(status).decode()
+        if status == GLIDE_EHIP:
+            msg += " (hipError %d)" % lib.glide_last_hip_error()
+        super().__init__("%s failed: %s" % (fn, msg))
+        self.status = status
+
+
+def load():
+    """Load libglide.so once; raises if it has not been built."""
+    global _lib
+    if _lib is not None:
+        return _lib
+    if not os.path.exists(LIB_PATH):
+        raise RuntimeError("libglide.so is not built: run `python -m paper_2402_02082_amd.build`")
+    lib = ctypes.CDLL(LIB_PATH)
+    P, I, F, Z = ctypes.c_void_p, ctypes.c_int, ctypes.c_float, ctypes.c_size_t
+    lib.glide_strerror.restype = ctypes.c_char_p
+    lib.glide_strerror.argtypes = [I]
+    lib.glide_last_hip_error.restype = I
+    lib.glide_last_hip_error.argtypes = []
+    lib.glide_tree_attn_workspace.restype = Z
+    lib.glide_tree_attn_workspace.argtypes = [I, I, I, I, I, I]
+    lib.glide_tree_attn.restype = I
+    lib.glide_tree_attn.argtypes = [P, P, P, P, P, P, I, I, I, I, I, I, F, I, P, Z, P]
+    lib.cape_expand_workspace.restype = Z
+    lib.cape_expand_workspace.argtypes = [I, I]
+    lib.cape_expand.restype = I
+    lib.cape_expand.argtypes = [P, I, I, I, I, I, I, P, P, P, P, Z, P]
+    lib.glide_argmax_rows.restype = I
+    lib.glide_argmax_rows.argtypes = [P, I, I, P, P]
+    lib.tree_verify.restype = I
+    lib.tree_verify.argtypes = [P, P, P, I, I, P, P, P, P]
+    _lib = lib
+    return lib
+
+
+EXPORTED = ["glide_strerror", "glide_last_hip_error", "glide_tree_attn_workspace",
+            "glide_tree_attn", "cape_expand_workspace", "cape_expand",
+            "glide_argmax_rows", "tree_verify"]
+
+
+def _ptr(t):
+    return None if t is None else ctypes.c_void_p(t.data_ptr())
+
+
+def _stream(stream, device):
+    if stream is None:
+        stream = torch.cuda.current_stream(device)
+    return ctypes.c_void_p(stream.cuda_stream)
+
+
+def _check(fn, status):
+    if status != GLIDE_OK:
+        raise GlideError(fn, status)
+
+
+def _need(cond, what):
+    if not cond:
+        raise ValueError(what)
+
+
+def _dev(t, name, dtype=None):
+    _need(isinstance(t, torch.Tensor), "%s must be a torch tensor" % name)
+    _need(t.is_cuda, "%s must be on the GPU" % name)
+    _need(t.is_contiguous(), "%s must be contiguous" % name)
+    if dtype is not None:
+        _need(t.dtype == dtype, "%s must be %s" % (name, dtype))
+
+
+# Zero-filled workspaces, kept per (device, stream) so that calls that may run
+# concurrently on different streams never share completion counters.
+_ws_cache = {}
+
+
+def attn_workspace(B, N, H, L_cap, max_splits, device, stream=None):
+    need = load().glide_tree_attn_workspace(B, N, H, HEAD_DIM, L_cap, max_splits)
+    if need == 0:
+        return None
+    s = torch.cuda.current_stream(device) if stream is None else stream
+    key = (str(device), s.cuda_stream)
+    ws = _ws_cache.get(key)
+    if ws is None or ws.numel() < need:
+        ws = torch.zeros(need, dtype=torch.uint8, device=device)
+        _ws_cache[key] = ws
+    return ws
+
+
+def glide_tree_attn(q, k_cache, v_cache, seq_lens, tree_parents, out, scale=0.0,
+                    max_splits=0, workspace=None, stream=None):
+    """out[b, n, h] = attention of q[b, n, h] over the prefix (and, with
+    tree_parents, the node's ancestor-or-self tree rows).  See include/glide.h."""
+    _dev(q, "q")
+    _need(q.dtype in (torch.bfloat16, torch.float32), "q must be bfloat16 or float32")
+    for name, t in (("k_cache", k_cache), ("v_cache", v_cache), ("out", out)):
+        _dev(t, name, q.dtype)
+    _dev(seq_lens, "seq_lens", torch.int32)
+    B, N, H, D = q.shape
+    _need(k_cache.dim() == 4 and k_cache.shape[:2] == (B, H) and k_cache.shape[3] == D,
+          "k_cache must be [B, H, L_cap, D]")
+    _need(v_cache.shape == k_cache.shape, "v_cache must match k_cache")
+    _need(out.shape == q.shape, "out must match q")
+    _need(seq_lens.shape == (B,), "seq_lens must be [B]")
+    if tree_parents is not None:
+        _dev(tree_parents, "tree_parents", torch.int32)
+        _need(tree_parents.shape == (B, N), "tree_parents must be [B, N]")
+    L_cap = k_cache.shape[2]
+    dtype = GLIDE_BF16 if q.dtype == torch.bfloat16 else GLIDE_F32
+    if workspace is None:
+        workspace = attn_workspace(B, N, H, L_cap, max_splits, q.device, stream)
+    ws_bytes = 0 if workspace is None else workspace.numel() * workspace.element_size()
+    status = load().glide_tree_attn(
+        _ptr(q), _ptr(k_cache), _ptr(v_cache), _ptr(seq_lens), _ptr(tree_parents), _ptr(out),
+        B, N, H, D, L_cap, dtype, float(scale), int(max_splits), _ptr(workspace), ws_bytes,
+        _stream(stream, q.device))
+    _check("glide_tree_attn", status)
+    return out
+
+
+def cape_expand(draft_probs, k, n_max, tokens_out, parents_out, n_nodes_out, fixed=False,
+                workspace=None, stream=None):
+    """CaPE expansion of draft_probs [B, gamma, V] into a parent-indexed tree."""
+    _dev(draft_probs, "draft_probs", torch.float32)
+    B, gamma, V = draft_probs.shape
+    for name, t, shape in (("tokens_out", tokens_out, (B, n_max)),
+                           ("parents_out", parents_out, (B, n_max)),
+                           ("n_nodes_out", n_nodes_out, (B,))):
+        _dev(t, name, torch.int32)
+        _need(tuple(t.shape) == shape, "%s must be %s" % (name, shape))
+    need = load().cape_expand_workspace(B, gamma)
+    if workspace is None:
+        workspace = torch.empty(max(need, 1), dtype=torch.uint8, device=draft_probs.device)
+    status = load().cape_expand(
+        _ptr(draft_probs), B, gamma, V, int(k), 1 if fixed else 0, int(n_max), _ptr(tokens_out),
+        _ptr(parents_out), _ptr(n_nodes_out), _ptr(workspace),
+        workspace.numel() * workspace.element_size(), _stream(stream, draft_probs.device))
+    _check("cape_expand", status)
+    return tokens_out, parents_out, n_nodes_out
+
+
+def glide_argmax_rows(logits, idx_out, stream=None):
+    """idx_out[r] = first index of the maximum of logits[r] (logits [..., V])."""
+    _dev(logits, "logits", torch.float32)
+    V = logits.shape[-1]
+    rows = logits.numel() // max(V, 1)
+    _dev(idx_out, "idx_out", torch.int32)
+    _need(idx_out.numel() == rows, "idx_out must have one entry per row")
+    status = load().glide_argmax_rows(_ptr(logits), rows, V, _ptr(idx_out),
+                                      _stream(stream, logits.device))
+    _check("glide_argmax_rows", status)
+    return idx_out
+
+
+def tree_verify(target_argmax, cand_tokens, parents, accept_len, last_node=None, bonus=None,
+                stream=None):
+    """Greedy acceptance: accept_len[b] (and optionally last_node, bonus)."""
+    _dev(cand_tokens, "cand_tokens", torch.int32)
+    B, N = cand_tokens.shape
+    _dev(target_argmax, "target_argmax", torch.int32)
+    _need(tuple(target_argmax.shape) == (B, N + 1), "target_argmax must be [B, N + 1]")
+    _dev(parents, "parents", torch.int32)
+    _need(tuple(parents.shape) == (B, N), "parents must be [B, N]")
+    for name, t in (("accept_len", accept_len), ("last_node", last_node), ("bonus", bonus)):
+        if t is not None:
+            _dev(t, name, torch.int32)
+            _need(tuple(t.shape) == (B,), "%s must be [B]" % name)
+    status = load().tree_verify(_ptr(target_argmax), _ptr(cand_tokens), _ptr(parents), B, N,
+                                _ptr(accept_len), _ptr(last_node), _ptr(bonus),
+                                _stream(stream, cand_tokens.device))
+    _check("tree_verify", status)
+    return accept_len

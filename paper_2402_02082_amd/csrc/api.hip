@@ -1,0 +1,168 @@
+// C ABI of libglide: argument checking, workspace planning and launches.
+// Every check that does not need device data runs before any HIP call, so
+// the error paths are testable on a machine without a GPU.
+#include <hip/hip_runtime.h>
+#include <math.h>
+#include <stdlib.h>
+#include <string.h>
+
+#include <vector>
+
+#include "glide.h"
+#include "internal.h"
+
+namespace {
+
+thread_local int g_last_hip_error = 0;
+
+int hip_status(hipError_t e) {
+  if (e == hipSuccess) return GLIDE_OK;
+  g_last_hip_error = (int)e;
+  return GLIDE_EHIP;
+}
+
+bool validate_enabled() {
+  const char* v = getenv("GLIDE_VALIDATE");
+  return v && v[0] && strcmp(v, "0") != 0;
+}
+
+// Copies a small int32 device array to the host (synchronises `stream`).
+bool fetch_ints(const int32_t* dev, size_t n, std::vector<int32_t>& host, hipStream_t stream,
+                int* status) {
+  host.resize(n);
+  hipError_t e = hipMemcpyAsync(host.data(), dev, n * sizeof(int32_t), hipMemcpyDeviceToHost, stream);
+  if (e == hipSuccess) e = hipStreamSynchronize(stream);
+  if (e != hipSuccess) {
+    *status = hip_status(e);
+    return false;
+  }
+  return true;
+}
+
+bool parents_ok(const std::vector<int32_t>& parents, int B, int N) {
+  for (int b = 0; b < B; ++b)
+    for (int n = 0; n < N; ++n) {
+      const int p = parents[(size_t)b * N + n];
+      if (p < -1 || p >= n) return false;
+    }
+  return true;
+}
+
+bool tree_attn_sizes_ok(int B, int N, int H, int D, int L_cap, bool tree) {
+  if (B < 1 || H < 1 || N < 1 || N > glide::kMaxNodes) return false;
+  if (D != glide::kHeadDim) return false;
+  if (L_cap < (tree ? N : 1)) return false;
+  // keep every element offset inside size_t and every key index inside int
+  if ((double)B * H * (double)L_cap * D > 9.0e18) return false;
+  return true;
+}
+
+}  // namespace
+
+extern "C" {
+
+const char* glide_strerror(int status) {
+  switch (status) {
+    case GLIDE_OK: return "ok";
+    case GLIDE_EINVAL: return "invalid argument";
+    case GLIDE_ERANGE: return "device data out of range";
+    case GLIDE_EHIP: return "HIP error";
+    default: return "unknown status";
+  }
+}
+
+int glide_last_hip_error(void) { return g_last_hip_error; }
+
+size_t glide_tree_attn_workspace(int B, int N, int H, int D, int L_cap, int max_splits) {
+  if (!tree_attn_sizes_ok(B, N, H, D, L_cap, false)) return 0;
+  if (max_splits < 0 || max_splits > glide::kMaxSplits) return 0;
+  return glide::plan_tree_attn(B, N, H, L_cap, max_splits).ws_bytes;
+}
+
+int glide_tree_attn(const void* q, const void* k_cache, const void* v_cache, const int32_t* seq_lens,
+                    const int32_t* tree_parents, void* out, int B, int N, int H, int D, int L_cap,
+                    int dtype, float scale, int max_splits, void* workspace, size_t ws_bytes,
+                    hipStream_t stream) {
+  const bool tree = tree_parents != nullptr;
+  if (!q || !k_cache || !v_cache || !seq_lens || !out) return GLIDE_EINVAL;
+  if (dtype != GLIDE_BF16 && dtype != GLIDE_F32) return GLIDE_EINVAL;
+  if (!tree_attn_sizes_ok(B, N, H, D, L_cap, tree)) return GLIDE_EINVAL;
+  if (max_splits < 0 || max_splits > glide::kMaxSplits) return GLIDE_EINVAL;
+  if (!isfinite(scale)) return GLIDE_EINVAL;
+  const glide::AttnPlan plan = glide::plan_tree_attn(B, N, H, L_cap, max_splits);
+  if (plan.ws_bytes > 0 && (!workspace || ws_bytes < plan.ws_bytes)) return GLIDE_EINVAL;
+
+  if (validate_enabled()) {
+    int status = GLIDE_OK;
+    std::vector<int32_t> lens, par;
+    if (!fetch_ints(seq_lens, (size_t)B, lens, stream, &status)) return status;
+    for (int b = 0; b < B; ++b)
+      if (lens[b] < 0 || lens[b] > L_cap - (tree ? N : 0)) return GLIDE_ERANGE;
+    if (tree) {
+      if (!fetch_ints(tree_parents, (size_t)B * N, par, stream, &status)) return status;
+      if (!parents_ok(par, B, N)) return GLIDE_ERANGE;
+    }
+  }
+
+  glide::AttnArgs a{};
+  a.q = q;
+  a.k = k_cache;
+  a.v = v_cache;
+  a.seq_lens = seq_lens;
+  a.parents = tree_parents;
+  a.out = out;
+  char* ws = (char*)workspace;
+  a.part_o = plan.ws_bytes ? (float*)(ws + plan.part_o_off) : nullptr;
+  a.part_ml = plan.ws_bytes ? (float2*)(ws + plan.part_ml_off) : nullptr;
+  a.counters = plan.ws_bytes ? (uint32_t*)(ws + plan.counter_off) : nullptr;
+  a.B = B;
+  a.N = N;
+  a.H = H;
+  a.L_cap = L_cap;
+  a.chunk = plan.chunk;
+  a.splits = plan.splits;
+  const double sc = scale > 0.f ? (double)scale : 1.0 / sqrt((double)D);
+  a.scale_log2 = (float)(sc * 1.4426950408889634);  // log2(e)
+  return hip_status(glide::launch_tree_attn(a, dtype == GLIDE_BF16, stream));
+}
+
+size_t cape_expand_workspace(int B, int gamma) {
+  if (B < 1 || gamma < 1 || gamma > glide::kMaxNodes) return 0;
+  return glide::cape_workspace_bytes(B, gamma);
+}
+
+int cape_expand(const float* draft_probs, int B, int gamma, int V, int k, int fixed, int n_max,
+                int32_t* tokens_out, int32_t* parents_out, int32_t* n_nodes_out, void* workspace,
+                size_t ws_bytes, hipStream_t stream) {
+  if (!draft_probs || !tokens_out || !parents_out || !n_nodes_out || !workspace) return GLIDE_EINVAL;
+  if (B < 1 || gamma < 1 || n_max < gamma || n_max > glide::kMaxNodes || V < 2) return GLIDE_EINVAL;
+  if (k < 0 || (fixed && k > GLIDE_CAPE_MAX_K)) return GLIDE_EINVAL;
+  if ((double)B * gamma * V > 9.0e18) return GLIDE_EINVAL;
+  if (ws_bytes < glide::cape_workspace_bytes(B, gamma)) return GLIDE_EINVAL;
+  return hip_status(glide::launch_cape_expand(draft_probs, B, gamma, V, k, fixed ? 1 : 0, n_max,
+                                              tokens_out, parents_out, n_nodes_out, workspace,
+                                              stream));
+}
+
+int glide_argmax_rows(const float* logits, int rows, int V, int32_t* idx_out, hipStream_t stream) {
+  if (!logits || !idx_out || rows < 1 || V < 1) return GLIDE_EINVAL;
+  if ((double)rows * V > 9.0e18) return GLIDE_EINVAL;
+  return hip_status(glide::launch_argmax_rows(logits, rows, V, idx_out, stream));
+}
+
+int tree_verify(const int32_t* target_argmax, const int32_t* cand_tokens, const int32_t* parents,
+                int B, int N, int32_t* accept_len, int32_t* last_node, int32_t* bonus,
+                hipStream_t stream) {
+  if (!target_argmax || !cand_tokens || !parents || !accept_len) return GLIDE_EINVAL;
+  if (B < 1 || N < 1 || N > glide::kMaxNodes) return GLIDE_EINVAL;
+  if (validate_enabled()) {
+    int status = GLIDE_OK;
+    std::vector<int32_t> par;
+    if (!fetch_ints(parents, (size_t)B * N, par, stream, &status)) return status;
+    if (!parents_ok(par, B, N)) return GLIDE_ERANGE;
+  }
+  return hip_status(glide::launch_tree_verify(target_argmax, cand_tokens, parents, B, N, accept_len,
+                                              last_node, bonus, stream));
+}
+
+}  // extern "C"

@@ -23,9 +23,11 @@ Recipe (seed s):
   1/2, ends on the first expansion token of position a; each logits row on the
   path gets the path token raised to (row max + 1), and the row after the
   path's last node gets a token that is none of that node's children;
-* Q, K and V are bfloat16 N(0, 1) (float32 in fp32 mode) from a torch
-  generator seeded with s, drawn layer by layer in the order K cache, V cache,
-  q.  Tree rows [L_b, L_b + N) of the cache are part of the same draw.
+* Q, K and V are bfloat16 N(0, 1) (float32 in fp32 mode) drawn in float32
+  from a torch generator seeded with 1000 s + layer, in the order K cache,
+  V cache, q; the GliDe cross-attention queries use layer index 999 and read
+  the last layer's cache.  Tree rows [L_b, L_b + N) of the cache are part of
+  the same draw.
 
 Nothing here calls the oracle or the HIP library.
 """
@@ -214,25 +216,32 @@ def torch_normal(shape, generator, dtype, device):
     return x.to(dtype)
 
 
-def attention_layers(wl, seed, dtype, device, layers=None, batch=None, heads=None,
-                     l_cap=None, n_q=None):
-    """Per-layer (q, k_cache, v_cache) tensors, drawn in the recipe's order.
+def layer_seed(seed, layer):
+    """Seed of one layer's tensors, so any layer can be drawn on its own."""
+    return int(seed) * 1000 + int(layer)
 
-    q [B, Nq, H, D]; caches [B, H, L_cap, D].  Returns a list of tuples.
-    """
+
+def attention_layer(wl, seed, layer, dtype, device, batch=None, heads=None, l_cap=None,
+                    n_q=None):
+    """(q, k_cache, v_cache) of one layer: q [B, Nq, H, D], caches
+    [B, H, L_cap, D], N(0, 1) drawn in the order K cache, V cache, q."""
     import torch
     g = torch.Generator(device=device)
-    g.manual_seed(int(seed))
-    L = wl.layers if layers is None else layers
+    g.manual_seed(layer_seed(seed, layer))
     B = wl.batch if batch is None else batch
     H = wl.heads if heads is None else heads
     Lc = wl.l_cap if l_cap is None else l_cap
     Nq = wl.nodes if n_q is None else n_q
     D = wl.head_dim
-    out = []
-    for _ in range(L):
-        k = torch_normal((B, H, Lc, D), g, dtype, device)
-        v = torch_normal((B, H, Lc, D), g, dtype, device)
-        q = torch_normal((B, Nq, H, D), g, dtype, device)
-        out.append((q, k, v))
-    return out
+    k = torch_normal((B, H, Lc, D), g, dtype, device)
+    v = torch_normal((B, H, Lc, D), g, dtype, device)
+    q = torch_normal((B, Nq, H, D), g, dtype, device)
+    return q, k, v
+
+
+def cross_queries(wl, seed, dtype, device):
+    """GliDe cross-attention queries [B, gamma, H, D] (one draft layer)."""
+    import torch
+    g = torch.Generator(device=device)
+    g.manual_seed(layer_seed(seed, 999))
+    return torch_normal((wl.batch, wl.depth, wl.heads, wl.head_dim), g, dtype, device)

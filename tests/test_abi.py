@@ -1,0 +1,125 @@
+"""CPU tests of the C ABI: the library loads, exports every symbol the header
+declares, and rejects bad arguments before any HIP call (so no GPU is needed)."""
+
+import ctypes
+import os
+import re
+
+import pytest
+
+import paper_2402_02082_amd as glide
+from paper_2402_02082_amd import _lib
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+HEADER = os.path.join(ROOT, "include", "glide.h")
+
+FAKE = ctypes.c_void_p(0x1000)  # never dereferenced: every call below fails validation
+
+
+def header_functions():
+    text = open(HEADER).read()
+    text = re.sub(r"/\*.*?\*/", "", text, flags=re.S)
+    return sorted(set(re.findall(r"^[A-Za-z_][\w\s\*]*?\b(\w+)\s*\(", text, flags=re.M)))
+
+
+@pytest.fixture(scope="module")
+def lib():
+    return _lib.load()
+
+
+def test_header_parses():
+    fns = header_functions()
+    assert {"glide_tree_attn", "cape_expand", "tree_verify", "glide_argmax_rows"} <= set(fns)
+
+
+def test_every_declared_symbol_is_exported(lib):
+    for name in header_functions():
+        assert hasattr(lib, name), name
+    assert sorted(header_functions()) == sorted(_lib.EXPORTED)
+
+
+def test_strerror(lib):
+    assert lib.glide_strerror(0) == b"ok"
+    assert lib.glide_strerror(glide.GLIDE_EINVAL) == b"invalid argument"
+    assert lib.glide_strerror(12345) == b"unknown status"
+    assert lib.glide_last_hip_error() == 0
+
+
+def _attn(lib, **kw):
+    a = dict(q=FAKE, k=FAKE, v=FAKE, lens=FAKE, parents=FAKE, out=FAKE, B=1, N=16, H=32, D=128,
+             L_cap=2064, dtype=0, scale=0.0, splits=0, ws=FAKE, ws_bytes=1 << 30)
+    a.update(kw)
+    return lib.glide_tree_attn(a["q"], a["k"], a["v"], a["lens"], a["parents"], a["out"], a["B"],
+                               a["N"], a["H"], a["D"], a["L_cap"], a["dtype"], a["scale"],
+                               a["splits"], a["ws"], a["ws_bytes"], None)
+
+
+@pytest.mark.parametrize("bad", [
+    dict(q=None), dict(k=None), dict(v=None), dict(lens=None), dict(out=None),
+    dict(N=0), dict(N=65), dict(D=64), dict(D=256), dict(B=0), dict(H=0), dict(dtype=2),
+    dict(dtype=-1), dict(L_cap=15), dict(splits=-1), dict(splits=65),
+    dict(scale=float("nan")), dict(scale=float("inf")), dict(ws=None), dict(ws_bytes=16),
+])
+def test_tree_attn_rejects(lib, bad):
+    assert _attn(lib, **bad) == glide.GLIDE_EINVAL
+
+
+def test_tree_attn_workspace_plan(lib):
+    # Vicuna-7B verify layer: 32 heads, 2048 + 16 keys -> a split plan with workspace
+    ws = lib.glide_tree_attn_workspace(1, 16, 32, 128, 2064, 0)
+    assert ws > 0
+    # one split needs no workspace
+    assert lib.glide_tree_attn_workspace(1, 16, 32, 128, 2064, 1) == 0
+    assert lib.glide_tree_attn_workspace(1, 16, 32, 128, 100, 0) == 0
+    # invalid sizes report 0
+    assert lib.glide_tree_attn_workspace(1, 65, 32, 128, 2064, 0) == 0
+    assert lib.glide_tree_attn_workspace(1, 16, 32, 64, 2064, 0) == 0
+    # more splits never need less workspace
+    sizes = [lib.glide_tree_attn_workspace(4, 32, 40, 128, 4128, s) for s in (2, 4, 8, 16, 32, 64)]
+    assert sizes == sorted(sizes)
+
+
+def _cape(lib, **kw):
+    a = dict(p=FAKE, B=1, gamma=5, V=32000, k=3, fixed=0, n_max=16, t=FAKE, par=FAKE, n=FAKE,
+             ws=FAKE, ws_bytes=1 << 20)
+    a.update(kw)
+    return lib.cape_expand(a["p"], a["B"], a["gamma"], a["V"], a["k"], a["fixed"], a["n_max"],
+                           a["t"], a["par"], a["n"], a["ws"], a["ws_bytes"], None)
+
+
+@pytest.mark.parametrize("bad", [
+    dict(p=None), dict(t=None), dict(par=None), dict(n=None), dict(ws=None), dict(B=0),
+    dict(gamma=0), dict(gamma=17), dict(n_max=65, gamma=5), dict(V=1), dict(k=-1),
+    dict(fixed=1, k=8), dict(ws_bytes=8),
+])
+def test_cape_rejects(lib, bad):
+    assert _cape(lib, **bad) == glide.GLIDE_EINVAL
+
+
+def test_cape_workspace(lib):
+    assert lib.cape_expand_workspace(2, 5) == 2 * 5 * 8 * 8
+    assert lib.cape_expand_workspace(0, 5) == 0
+    assert lib.cape_expand_workspace(1, 65) == 0
+
+
+@pytest.mark.parametrize("args", [
+    (None, 4, 10, FAKE), (FAKE, 0, 10, FAKE), (FAKE, 4, 0, FAKE), (FAKE, 4, 10, None),
+])
+def test_argmax_rejects(lib, args):
+    assert lib.glide_argmax_rows(*args, None) == glide.GLIDE_EINVAL
+
+
+@pytest.mark.parametrize("args", [
+    (None, FAKE, FAKE, 1, 8, FAKE), (FAKE, None, FAKE, 1, 8, FAKE), (FAKE, FAKE, None, 1, 8, FAKE),
+    (FAKE, FAKE, FAKE, 0, 8, FAKE), (FAKE, FAKE, FAKE, 1, 0, FAKE), (FAKE, FAKE, FAKE, 1, 65, FAKE),
+    (FAKE, FAKE, FAKE, 1, 8, None),
+])
+def test_verify_rejects(lib, args):
+    assert lib.tree_verify(*args, None, None, None) == glide.GLIDE_EINVAL
+
+
+def test_binding_rejects_host_tensors():
+    import torch
+    q = torch.zeros(1, 4, 2, 128, dtype=torch.bfloat16)
+    with pytest.raises(ValueError):
+        glide.glide_tree_attn(q, q, q, torch.zeros(1, dtype=torch.int32), None, q)

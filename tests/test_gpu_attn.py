@@ -1,0 +1,158 @@
+"""GPU parity of glide_tree_attn against the float64 oracle.
+
+Shapes span several 32-key steps and 128-key split chunks with ragged tails,
+every query-tile count (N = 1 .. 64), empty prefixes, cross mode, forced split
+counts and both element types.  Tolerances: max-abs 1e-2 (bf16 inputs, fp32
+accumulation) and 1e-5 (fp32 mode).
+"""
+
+import os
+
+import numpy as np
+import pytest
+import torch
+
+import paper_2402_02082_amd as glide
+from oracle import attention as OA
+from synth import workloads as W
+from tests.gpu_common import BF16_TOL, F32_TOL, cpu_normal, require_gpu, say, to64
+
+pytestmark = pytest.mark.gpu
+
+D = 128
+
+
+def _parents(kind, B, N, seed):
+    if kind is None:
+        return None
+    if kind == "chain":
+        return np.tile(np.arange(-1, N - 1, dtype=np.int32), (B, 1))
+    if kind == "roots":
+        return np.full((B, N), -1, dtype=np.int32)
+    if kind == "random":
+        return W.random_parents(B, N, 8, seed)
+    if kind == "cape":  # proposal chain of depth min(N, 8) then leaves on every position
+        g = min(N, 8)
+        p = [i - 1 for i in range(g)] + [((j - g) % g) - 1 for j in range(g, N)]
+        return np.tile(np.asarray(p, dtype=np.int32), (B, 1))
+    raise ValueError(kind)
+
+
+def run_case(B, N, H, lens, kind, dtype, splits, seed, l_cap=None):
+    require_gpu()
+    say("tree_attn", dict(B=B, N=N, H=H, lens=list(lens), kind=kind, dtype=str(dtype),
+                          splits=splits, seed=seed))
+    tree = kind is not None
+    L_cap = l_cap or (max(lens) + (N if tree else 0))
+    q = cpu_normal((B, N, H, D), seed, dtype)
+    k = cpu_normal((B, H, L_cap, D), seed + 1, dtype)
+    v = cpu_normal((B, H, L_cap, D), seed + 2, dtype)
+    parents = _parents(kind, B, N, seed)
+    dev = torch.device("cuda")
+    out = torch.empty((B, N, H, D), dtype=dtype, device=dev)
+    glide.glide_tree_attn(q.to(dev), k.to(dev), v.to(dev),
+                          torch.tensor(lens, dtype=torch.int32, device=dev),
+                          None if parents is None else torch.from_numpy(parents).to(dev),
+                          out, max_splits=splits)
+    torch.cuda.synchronize()
+    ref = OA.tree_attention(to64(q), to64(k), to64(v), lens, parents)
+    got = to64(out)
+    assert np.isfinite(got).all()
+    return got, ref
+
+
+CASES = [
+    # B, N, H, lens, kind, splits
+    (1, 5, 4, [512], "chain", 0),
+    (1, 5, 4, [512], "chain", 1),
+    (1, 16, 4, [2048], "cape", 0),
+    (1, 16, 2, [2048], "cape", 9),
+    (2, 17, 2, [33, 300], "random", 0),
+    (3, 32, 2, [0, 1, 129], "random", 2),
+    (2, 31, 2, [255, 256], "cape", 3),
+    (2, 33, 2, [257, 1000], "random", 7),
+    (1, 48, 2, [500], "random", 0),
+    (2, 63, 2, [127, 128], "random", 64),
+    (2, 64, 2, [4096, 1500], "cape", 0),
+    (1, 64, 2, [4096], "roots", 0),
+    (1, 1, 3, [1], "chain", 0),
+    (1, 1, 3, [777], "roots", 5),
+    (2, 5, 3, [1, 2048], None, 0),      # cross mode
+    (2, 5, 3, [31, 129], None, 2),
+    (1, 64, 2, [3000], None, 0),
+    (3, 8, 2, [0, 33, 64], None, 1),    # empty key set for b = 0
+]
+
+
+@pytest.mark.parametrize("dtype", [torch.bfloat16, torch.float32], ids=["bf16", "f32"])
+@pytest.mark.parametrize("case", CASES, ids=lambda c: "B%dN%dH%d-%s-%s-s%d" % (
+    c[0], c[1], c[2], "_".join(map(str, c[3])), c[4], c[5]))
+def test_parity(case, dtype):
+    B, N, H, lens, kind, splits = case
+    got, ref = run_case(B, N, H, lens, kind, dtype, splits, seed=17 + N)
+    tol = BF16_TOL if dtype == torch.bfloat16 else F32_TOL
+    err = float(np.abs(got - ref).max())
+    assert err <= tol, err
+
+
+@pytest.mark.parametrize("dtype", [torch.bfloat16, torch.float32], ids=["bf16", "f32"])
+def test_single_visible_key_is_exact(dtype):
+    """Empty prefix, every node a root: each row sees only its own value row,
+    so the output is that row exactly (weight 1)."""
+    got, ref = run_case(2, 40, 3, [0, 0], "roots", dtype, 0, seed=5, l_cap=40)
+    assert np.array_equal(got, ref)
+
+
+def test_empty_cross_key_set_is_zero():
+    got, _ = run_case(2, 5, 2, [0, 0], None, torch.bfloat16, 0, seed=6, l_cap=64)
+    assert not got.any()
+
+
+def test_ragged_l_cap_slack():
+    """L_cap well above the longest prefix: the unused rows are never read."""
+    require_gpu()
+    got, ref = run_case(2, 20, 2, [100, 333], "random", torch.bfloat16, 0, seed=7, l_cap=4096)
+    assert float(np.abs(got - ref).max()) <= BF16_TOL
+
+
+def test_deterministic_and_split_invariant():
+    require_gpu()
+    dev = torch.device("cuda")
+    B, N, H, L = 2, 32, 4, 3000
+    q = cpu_normal((B, N, H, D), 1, torch.bfloat16).to(dev)
+    k = cpu_normal((B, H, L + N, D), 2, torch.bfloat16).to(dev)
+    v = cpu_normal((B, H, L + N, D), 3, torch.bfloat16).to(dev)
+    lens = torch.tensor([L, L - 777], dtype=torch.int32, device=dev)
+    par = torch.from_numpy(W.random_parents(B, N, 6, 4)).to(dev)
+    outs = {}
+    for splits in (1, 2, 5, 16, 64, 0, 0):
+        o = torch.empty((B, N, H, D), dtype=torch.bfloat16, device=dev)
+        glide.glide_tree_attn(q, k, v, lens, par, o, max_splits=splits)
+        outs.setdefault(splits, []).append(o)
+    torch.cuda.synchronize()
+    assert torch.equal(outs[0][0], outs[0][1])
+    base = outs[1][0].float()
+    for s, os_ in outs.items():
+        assert float((os_[0].float() - base).abs().max()) <= BF16_TOL
+
+
+def test_validation_reports_bad_device_data(monkeypatch):
+    require_gpu()
+    dev = torch.device("cuda")
+    q = torch.zeros((1, 4, 2, D), dtype=torch.bfloat16, device=dev)
+    k = torch.zeros((1, 2, 64, D), dtype=torch.bfloat16, device=dev)
+    out = torch.empty_like(q)
+    monkeypatch.setenv("GLIDE_VALIDATE", "1")
+    bad_parents = torch.tensor([[-1, 0, 3, 1]], dtype=torch.int32, device=dev)
+    lens = torch.tensor([10], dtype=torch.int32, device=dev)
+    with pytest.raises(glide.GlideError) as e:
+        glide.glide_tree_attn(q, k, k, lens, bad_parents, out)
+    assert e.value.status == glide.GLIDE_ERANGE
+    with pytest.raises(glide.GlideError) as e:
+        glide.glide_tree_attn(q, k, k, torch.tensor([61], dtype=torch.int32, device=dev),
+                              torch.tensor([[-1, 0, 1, 2]], dtype=torch.int32, device=dev), out)
+    assert e.value.status == glide.GLIDE_ERANGE
+    # valid data passes validation
+    glide.glide_tree_attn(q, k, k, lens, torch.tensor([[-1, 0, 1, 1]], dtype=torch.int32,
+                                                       device=dev), out)
+    torch.cuda.synchronize()
