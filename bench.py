@@ -18,8 +18,11 @@ batch 1, prefix 2048, 16-node CaPE tree of depth 5 with top-k 3) plus one
 5-query GliDe cross-attention layer.
 
 Prints one JSON line.  `value` is the attention bytes per step (K/V rows read,
-Q read, O written; the algorithmic count, split partials excluded) divided by
-the wall time of the whole step.
+Q read, O written in every attention call of the step; the algorithmic count,
+split partials excluded) divided by the GPU time of the whole step, replayed
+as a HIP graph so that host launch overhead is not timed.  `roofline` is the
+verification attention call (attention kernel + split merge) timed with HIP
+events around each call.
 """
 
 import argparse
@@ -88,18 +91,21 @@ class Step:
         self.ws = glide.attn_workspace(B, N, wl.heads, L_cap, max_splits, dev)
         self.xws = (glide.attn_workspace(B, wl.depth, wl.heads, L_cap, max_splits, dev)
                     if wl.cross else None)
+        self.cape_ws = torch.empty(max(glide.load().cape_expand_workspace(B, wl.depth), 1),
+                                   dtype=torch.uint8, device=dev)
         elem = 2 if dtype == torch.bfloat16 else 4
         self.verify_bytes = attn_bytes(self.lens_np, N, wl.heads, elem, True)
         self.cross_bytes = attn_bytes(self.lens_np, wl.depth, wl.heads, elem, False) \
             if wl.cross else 0
 
-    def run(self, attn_events=None):
-        wl = self.wl
+    def tree(self):
         if self.probs is not None:
-            glide.cape_expand(self.probs, wl.k, wl.nodes, self.tokens, self.parents, self.n_nodes)
-            tokens, parents = self.tokens, self.parents
-        else:
-            tokens, parents = self.chain_tokens, self.chain_parents
+            return self.tokens, self.parents
+        return self.chain_tokens, self.chain_parents
+
+    def run_verify_layers(self, attn_events=None):
+        """The verification pass's attention: one call per target layer."""
+        _, parents = self.tree()
         for i, ((q, k, v), o) in enumerate(zip(self.layers, self.outs)):
             if attn_events is not None:
                 attn_events[i][0].record()
@@ -107,6 +113,14 @@ class Step:
                                   workspace=self.ws)
             if attn_events is not None:
                 attn_events[i][1].record()
+
+    def run(self):
+        wl = self.wl
+        if self.probs is not None:
+            glide.cape_expand(self.probs, wl.k, wl.nodes, self.tokens, self.parents, self.n_nodes,
+                              workspace=self.cape_ws)
+        tokens, parents = self.tree()
+        self.run_verify_layers()
         glide.glide_argmax_rows(self.logits, self.ta)
         glide.tree_verify(self.ta, tokens, parents, self.acc, self.last, self.bonus)
         if wl.cross:
@@ -183,6 +197,9 @@ def main():
     ap.add_argument("--workload", type=int, default=2, choices=sorted(W.WORKLOADS))
     ap.add_argument("--max-splits", type=int, default=0)
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--calibrate-copy-mib", type=int, default=0,
+                    help="only run a plain device-to-device copy of this many MiB (five times), "
+                         "for scaling HBM traffic counters; prints nothing else")
     args = ap.parse_args()
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
         print("bench.py measures one GPU only: the hot path here is a single-GPU kernel set and "
@@ -191,6 +208,15 @@ def main():
     if not torch.cuda.is_available():
         print("bench.py needs a GPU", file=sys.stderr)
         sys.exit(2)
+    if args.calibrate_copy_mib:
+        n = args.calibrate_copy_mib << 20
+        src = torch.ones(n, dtype=torch.uint8, device="cuda")
+        dst = torch.empty_like(src)
+        for _ in range(5):
+            dst.copy_(src)
+        torch.cuda.synchronize()
+        print(json.dumps({"copy_bytes": n, "copies": 5}), flush=True)
+        return
     glide.load()
 
     wl = W.WORKLOADS[args.workload]
@@ -198,34 +224,58 @@ def main():
     step = Step(wl, dtype, SEED, args.max_splits)
     torch.cuda.synchronize()
 
-    for _ in range(args.warmup):
+    # Capture one whole step, and the verification layers alone, as HIP
+    # graphs (the library never allocates, so both replay as captured).
+    side = torch.cuda.Stream()
+    side.wait_stream(torch.cuda.current_stream())
+    with torch.cuda.stream(side):
+        for _ in range(max(args.warmup, 1)):
+            step.run()
+    torch.cuda.current_stream().wait_stream(side)
+    torch.cuda.synchronize()
+    g_step, g_verify = torch.cuda.CUDAGraph(), torch.cuda.CUDAGraph()
+    with torch.cuda.graph(g_step):
         step.run()
+    with torch.cuda.graph(g_verify):
+        step.run_verify_layers()
+    torch.cuda.synchronize()
+    for _ in range(args.warmup):
+        g_step.replay()
     torch.cuda.synchronize()
 
-    # Timed region: K whole steps, per-launch events on the attention kernels.
-    ev = [[(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True))
-           for _ in range(wl.layers)] for _ in range(args.steps)]
+    # Timed region 1: K whole steps (graph replays).
     start, stop = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
-    torch.cuda.synchronize()
     start.record()
-    for i in range(args.steps):
-        step.run(ev[i])
+    for _ in range(args.steps):
+        g_step.replay()
     stop.record()
     torch.cuda.synchronize()
     ms_step = start.elapsed_time(stop) / args.steps
-    per_launch = [a.elapsed_time(b) for e in ev for a, b in e]
-    launch_ms = float(np.mean(per_launch))
-    verify_us = float(np.mean([ev[i][0][0].elapsed_time(ev[i][-1][1])
-                               for i in range(args.steps)])) * 1e3
-
-    # Untimed check that the last step produced the planted acceptance.
     acc = step.acc.cpu().numpy()
     planted_ok = bool(np.array_equal(acc, step.planted))
 
-    step_bytes = step.verify_bytes + step.cross_bytes
+    # Timed region 2: the verification step alone (the L attention calls).
+    start.record()
+    for _ in range(args.steps):
+        g_verify.replay()
+    stop.record()
+    torch.cuda.synchronize()
+    verify_us = start.elapsed_time(stop) / args.steps * 1e3
+
+    # Timed region 3: per-call events around each verification attention call
+    # (attention kernel + split merge), issued eagerly behind a GPU sleep so
+    # the queue is already full and the events bracket GPU time only.
+    ev = [[(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True))
+           for _ in range(wl.layers)] for _ in range(args.steps)]
+    torch.cuda._sleep(int(2e8))
+    for i in range(args.steps):
+        step.run_verify_layers(ev[i])
+    torch.cuda.synchronize()
+    call_ms = float(np.mean([a.elapsed_time(b) for e in ev for a, b in e]))
+
+    step_bytes = step.verify_bytes * wl.layers + step.cross_bytes
     value = step_bytes / (ms_step * 1e-3) / 1e9
-    per_launch_bytes = step.verify_bytes / wl.layers
-    achieved = per_launch_bytes / (launch_ms * 1e-3) / 1e9
+    achieved = step.verify_bytes / (call_ms * 1e-3) / 1e9
     rec = {
         "metric": METRIC,
         "value": round(value, 3),
@@ -245,14 +295,16 @@ def main():
                    "tree_depth": wl.depth, "top_k": wl.k, "vocab": wl.vocab,
                    "cross_attn_queries": wl.depth if wl.cross else 0, "seed": SEED},
         "us_per_verify_step": round(verify_us, 2),
+        "verify_step_gbps": round(step.verify_bytes * wl.layers / (verify_us * 1e-6) / 1e9, 2),
         "hbm_frac_of_step": round(value / HBM_PEAK_GBPS, 4),
         "planted_accept_len_ok": planted_ok,
         "roofline": {"bound": "hbm", "achieved": round(achieved, 2), "peak": HBM_PEAK_GBPS,
                      "unit": "GB/s", "frac": round(achieved / HBM_PEAK_GBPS, 4),
                      "traffic": load_traffic(),
-                     "kernel": "tree_attn_kernel (verification, per layer)",
-                     "bytes_per_launch": per_launch_bytes,
-                     "avg_launch_us": round(launch_ms * 1e3, 3)},
+                     "kernel": "glide_tree_attn call (tree_attn_kernel + tree_attn_combine), "
+                               "verification layer",
+                     "bytes_per_launch": step.verify_bytes,
+                     "avg_launch_us": round(call_ms * 1e3, 3)},
     }
     if not args.no_cpu_baseline:
         rec["cpu_baseline"] = cpu_baseline(step)

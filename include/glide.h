@@ -72,10 +72,11 @@ int glide_last_hip_error(void);
 /*
  * Workspace bytes glide_tree_attn needs for these sizes (0 when the call runs
  * without a workspace, i.e. with one split).  Arguments as glide_tree_attn.
- * The workspace holds per-split partial softmax states and one completion
- * counter per (sequence, head).  It must be zero-filled ONCE after allocation
- * (every call leaves the counters at zero again) and must not be shared by
- * calls that can run concurrently.  Returns 0 for invalid sizes as well.
+ * The workspace holds the per-split partial softmax states (running max,
+ * running sum and unnormalised output of every query row); each call writes
+ * them before reading them, so no initialisation is needed and one buffer of
+ * the largest size needed can serve calls of any shape in turn.  It must not
+ * be shared by calls that can run concurrently.  Returns 0 for invalid sizes.
  */
 size_t glide_tree_attn_workspace(int B, int N, int H, int D, int L_cap,
                                  int max_splits);
@@ -107,8 +108,8 @@ size_t glide_tree_attn_workspace(int B, int N, int H, int D, int L_cap,
  *   dtype        GLIDE_BF16 or GLIDE_F32.
  *   scale        softmax scale; <= 0 selects 1/sqrt(D).
  *   max_splits   0 = choose automatically, else 1..64 key-range splits.
- *   workspace    device buffer of >= glide_tree_attn_workspace(...) bytes,
- *                zero-filled once; may be NULL when that size is 0.
+ *   workspace    device buffer of >= glide_tree_attn_workspace(...) bytes;
+ *                may be NULL when that size is 0.
  */
 int glide_tree_attn(const void* q, const void* k_cache, const void* v_cache,
                     const int32_t* seq_lens, const int32_t* tree_parents,

@@ -93,8 +93,8 @@ def _dev(t, name, dtype=None):
         _need(t.dtype == dtype, "%s must be %s" % (name, dtype))
 
 
-# Zero-filled workspaces, kept per (device, stream) so that calls that may run
-# concurrently on different streams never share completion counters.
+# Workspaces, kept per (device, stream) so that calls that may run
+# concurrently on different streams never share partial states.
 _ws_cache = {}
 
 
@@ -106,7 +106,7 @@ def attn_workspace(B, N, H, L_cap, max_splits, device, stream=None):
     key = (str(device), s.cuda_stream)
     ws = _ws_cache.get(key)
     if ws is None or ws.numel() < need:
-        ws = torch.zeros(need, dtype=torch.uint8, device=device)
+        ws = torch.empty(need, dtype=torch.uint8, device=device)
         _ws_cache[key] = ws
     return ws
 

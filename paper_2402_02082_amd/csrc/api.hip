@@ -114,7 +114,6 @@ int glide_tree_attn(const void* q, const void* k_cache, const void* v_cache, con
   char* ws = (char*)workspace;
   a.part_o = plan.ws_bytes ? (float*)(ws + plan.part_o_off) : nullptr;
   a.part_ml = plan.ws_bytes ? (float2*)(ws + plan.part_ml_off) : nullptr;
-  a.counters = plan.ws_bytes ? (uint32_t*)(ws + plan.counter_off) : nullptr;
   a.B = B;
   a.N = N;
   a.H = H;

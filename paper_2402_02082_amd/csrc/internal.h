@@ -11,14 +11,15 @@ constexpr int kHeadDim = 128;
 constexpr int kMaxNodes = 64;
 constexpr int kMaxSplits = 64;
 constexpr int kNumCU = 256;        // MI355X compute units (split heuristic)
-constexpr int kChunkQuantum = 128; // split boundaries are multiples of this
+constexpr int kChunkQuantum = 32;  // split boundaries are multiples of this
+constexpr int kMinChunk = 128;     // smallest split the automatic plan makes
 
 // How the keys of one (sequence, head) are divided between workgroups.
 struct AttnPlan {
   int splits;       // workgroups per (sequence, head)
   int chunk;        // keys per workgroup (multiple of kChunkQuantum)
-  size_t ws_bytes;  // workspace for partial states + counters (0 if splits == 1)
-  size_t part_o_off, part_ml_off, counter_off;
+  size_t ws_bytes;  // workspace for the partial states (0 if splits == 1)
+  size_t part_o_off, part_ml_off;
 };
 
 AttnPlan plan_tree_attn(int B, int N, int H, int L_cap, int max_splits);
@@ -32,7 +33,6 @@ struct AttnArgs {
   void* out;
   float* part_o;           // [B, H, splits, N, D]
   float2* part_ml;         // [B, H, splits, N] (running max in log2 units, sum)
-  uint32_t* counters;      // [B, H]
   int B, N, H, L_cap, chunk, splits;
   float scale_log2;        // softmax scale * log2(e)
 };

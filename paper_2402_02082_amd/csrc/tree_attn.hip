@@ -10,8 +10,11 @@
 //
 // Work decomposition: one workgroup (4 waves) per (split, head, sequence).
 // A split owns a contiguous key range; its waves take interleaved 32-key
-// steps (16 for float32), so every K/V byte is read from HBM exactly once and
-// is shared by all query rows of the sequence inside the MFMA tiles.
+// steps (16 for float32), so every K/V byte is read from HBM once and is
+// shared by all query rows of the sequence inside the MFMA tiles.  Up to 32
+// query rows (two 16-row tiles) each wave covers all of them; for 33..64 rows
+// the waves form two groups of two, one per pair of tiles, and each K/V step
+// is fetched by both groups (the second read hits L2).
 //
 // Per step and wave (bf16):
 //   S^T[key, query] = K Q^T   on v_mfma_f32_16x16x32_bf16, A = 16 key rows
@@ -27,10 +30,10 @@
 // Tree masking is only evaluated in steps that reach the tree rows, from a
 // 64-bit ancestor mask per query built by pointer doubling over the parents.
 //
-// The four waves merge their (max, sum, O) states through LDS; with more than
-// one split the workgroup writes a partial state, and the last workgroup of a
-// (sequence, head) to finish (a device-scope counter) merges all partials in
-// a fixed split order and resets the counter.
+// Each wave keeps two or three steps of K/V loads in flight in registers.
+// The four waves merge their (max, sum, O) states through LDS.  With more
+// than one split per (sequence, head) each workgroup writes a partial state
+// and a second small kernel merges the partials in a fixed split order.
 #include <hip/hip_runtime.h>
 #include <stdint.h>
 
@@ -73,17 +76,17 @@ __device__ __forceinline__ uint64_t shfl_u64(uint64_t v, int src) {
 }
 
 // Ancestor-or-self bitmask of node `lane` (bit m set iff tree node m is the
-// node itself or one of its ancestors).  Pointer doubling: after round r the
-// mask covers ancestors closer than 2^r and `p` points 2^r levels up; six
-// rounds cover any depth <= 64.  Parents outside [-1, lane) count as -1.
-__device__ __forceinline__ uint64_t ancestor_mask(const int32_t* parents_b, int N,
-                                                  int lane) {
-  int p = -1;
+// node itself or one of its ancestors), from that node's parent index.
+// Pointer doubling: after round r the mask covers ancestors closer than 2^r
+// and `p` points 2^r levels up; six rounds cover any depth <= 64.  Parents
+// outside [-1, lane) count as -1.
+__device__ __forceinline__ uint64_t ancestor_mask_from(int p, int N, int lane) {
   uint64_t a = 0;
   if (lane < N) {
-    p = parents_b[lane];
     if (p < -1 || p >= lane) p = -1;
     a = 1ull << lane;
+  } else {
+    p = -1;
   }
 #pragma unroll
   for (int round = 0; round < 6; ++round) {
@@ -157,61 +160,119 @@ __device__ __forceinline__ void load_q<F32Path>(F32Path::QFrag& f, const float* 
     f.v[e] = valid ? *(const f32x4_t*)(qrow + 32 * g + 4 * e) : f32x4_t{0.f, 0.f, 0.f, 0.f};
 }
 
-__device__ __forceinline__ void load_kv(Bf16Path::KV& f, const uint16_t* kp, const uint16_t* vp,
-                                        int j0, int kmax, int c, int g) {
+// K/V rows are fetched with buffer loads.  For each step the descriptor
+// starts at the step's first key row and ends at the split's last key, so
+// rows past the split read as zeros without touching memory (the partial
+// last step and padding steps need no clamping and never see other splits'
+// or uninitialised rows), the per-lane offsets stay fixed for the whole loop
+// and the per-step part of the address lives in scalar registers.
+// Word 3 of a gfx9 buffer descriptor: data format 32 bits (bits 15..18 = 4),
+// no swizzle, raw (unstrided) addressing.
+constexpr int kBufferDesc3 = 0x00020000;
+
+__device__ __forceinline__ __amdgpu_buffer_rsrc_t step_rsrc(const char* slab, int j0, int k_end,
+                                                            int row_bytes) {
+  const int rows = max(k_end - j0, 0);
+  return __builtin_amdgcn_make_buffer_rsrc(const_cast<char*>(slab) + (size_t)j0 * row_bytes,
+                                           (short)0, rows * row_bytes, kBufferDesc3);
+}
+
+__device__ __forceinline__ u32x4_t load16(__amdgpu_buffer_rsrc_t r, int off) {
+  return __builtin_bit_cast(u32x4_t, __builtin_amdgcn_raw_buffer_load_b128(r, off, 0, 0));
+}
+
+// Per-lane byte offsets inside one step, fixed for the whole loop.
+struct LaneOffsets {
+  int k0, k1;  // K rows
+  int v0, v1;  // V rows
+};
+
+// bf16 (row = 256 bytes).  K: lane (c, g) reads rows 16*kt + c at bytes
+// 64*st + 16*g; V: rows key_slot(g, i) = 16*(i / 4) + 4*g + i % 4 at 16*c.
+__device__ __forceinline__ LaneOffsets lane_offsets(Bf16Path, int c, int g) {
+  return LaneOffsets{c * 256 + 16 * g, (16 + c) * 256 + 16 * g, (4 * g) * 256 + 16 * c,
+                     (16 + 4 * g) * 256 + 16 * c};
+}
+
+__device__ __forceinline__ void load_kv(Bf16Path::KV& f, const char* kslab, const char* vslab,
+                                        int j0, int k_end, const LaneOffsets& o) {
+  const __amdgpu_buffer_rsrc_t rk = step_rsrc(kslab, j0, k_end, 256);
+  const __amdgpu_buffer_rsrc_t rv = step_rsrc(vslab, j0, k_end, 256);
 #pragma unroll
-  for (int kt = 0; kt < 2; ++kt) {
-    const int row = min(j0 + 16 * kt + c, kmax);
-#pragma unroll
-    for (int st = 0; st < 4; ++st)
-      f.k[kt][st] = *(const u32x4_t*)(kp + (size_t)row * kD + 32 * st + 8 * g);
+  for (int st = 0; st < 4; ++st) {
+    f.k[0][st] = load16(rk, o.k0 + 64 * st);
+    f.k[1][st] = load16(rk, o.k1 + 64 * st);
   }
 #pragma unroll
-  for (int i = 0; i < 8; ++i) {
-    const int row = min(j0 + Bf16Path::key_slot(g, i), kmax);
-    f.v[i] = *(const u32x4_t*)(vp + (size_t)row * kD + 8 * c);
+  for (int i = 0; i < 4; ++i) {
+    f.v[i] = load16(rv, o.v0 + 256 * i);
+    f.v[4 + i] = load16(rv, o.v1 + 256 * i);
   }
 }
 
-__device__ __forceinline__ void load_kv(F32Path::KV& f, const float* kp, const float* vp, int j0,
-                                        int kmax, int c, int g) {
-  const int krow = min(j0 + c, kmax);
+// float32 (row = 512 bytes).  K: row c at bytes 128*g + 16*e; V: rows
+// 4*g + r at bytes 32*c + 16*h.
+__device__ __forceinline__ LaneOffsets lane_offsets(F32Path, int c, int g) {
+  return LaneOffsets{c * 512 + 128 * g, 0, (4 * g) * 512 + 32 * c, 0};
+}
+
+__device__ __forceinline__ void load_kv(F32Path::KV& f, const char* kslab, const char* vslab, int j0,
+                                        int k_end, const LaneOffsets& o) {
+  const __amdgpu_buffer_rsrc_t rk = step_rsrc(kslab, j0, k_end, 512);
+  const __amdgpu_buffer_rsrc_t rv = step_rsrc(vslab, j0, k_end, 512);
 #pragma unroll
-  for (int e = 0; e < 8; ++e) f.k[e] = *(const f32x4_t*)(kp + (size_t)krow * kD + 32 * g + 4 * e);
+  for (int e = 0; e < 8; ++e) f.k[e] = __builtin_bit_cast(f32x4_t, load16(rk, o.k0 + 16 * e));
 #pragma unroll
-  for (int r = 0; r < 4; ++r) {
-    const int row = min(j0 + 4 * g + r, kmax);
+  for (int r = 0; r < 4; ++r)
 #pragma unroll
-    for (int h = 0; h < 2; ++h) f.v[r][h] = *(const f32x4_t*)(vp + (size_t)row * kD + 8 * c + 4 * h);
-  }
+    for (int h = 0; h < 2; ++h)
+      f.v[r][h] = __builtin_bit_cast(f32x4_t, load16(rv, o.v0 + 512 * r + 16 * h));
 }
 
 // Online-softmax state of one 16-query tile for the lane's query column.
+// The reference max `m` is moved lazily: only when a new score exceeds it
+// by more than kRescaleSlack (log2 units) are the accumulators rescaled, so
+// probabilities stay <= 2^kRescaleSlack and most steps skip the rescale.
+constexpr float kRescaleSlack = 8.f;
+
 struct SoftmaxState {
-  float m;  // running max of scaled scores (log2 units)
-  float l;  // running sum of exp2(score - m) over this lane's keys
+  float m;  // reference max of scaled scores (log2 units); -inf until a key is seen
+  float l;  // sum of exp2(score - m) over this lane's keys
 };
 
-// Scores of one step for one query tile -> masked, scaled, exponentiated.
-// x[] holds S^T values for keys key_of(idx) of this lane; returns the
-// rescale factor of the accumulators and leaves probabilities in x[].
+// Given the raw scores x[] of this lane's keys for one query tile (masked
+// ones -inf), decide whether the wave moves its reference max, rescale if so,
+// and turn x[] into probabilities exp2(x * scale_log2 - m).  The max is taken
+// over the rounded scaled scores themselves, so the largest score of a row
+// gets probability exactly 1.  Returns true when the accumulators must be
+// rescaled by `alpha`.
 template <int NV>
-__device__ __forceinline__ float softmax_step(float (&x)[NV], SoftmaxState& st) {
+__device__ __forceinline__ bool softmax_update(float (&x)[NV], SoftmaxState& st, float scale_log2,
+                                               float& alpha) {
+#pragma unroll
+  for (int i = 0; i < NV; ++i) x[i] *= scale_log2;
   float mx = x[0];
 #pragma unroll
   for (int i = 1; i < NV; ++i) mx = fmaxf(mx, x[i]);
   mx = max_across_groups(mx);
-  const float m_new = fmaxf(st.m, mx);
-  const float m_ref = (m_new == neg_inf()) ? 0.f : m_new;
-  const float alpha = fast_exp2(st.m - m_ref);
+  const bool move = __any(mx > st.m + kRescaleSlack);
+  alpha = 1.f;
+  if (move) {
+    const float m_new = fmaxf(st.m, mx);
+    alpha = (m_new == neg_inf()) ? 1.f : fast_exp2(st.m - m_new);
+    st.m = m_new;
+    st.l *= alpha;
+  }
+  const float m_ref = (st.m == neg_inf()) ? 0.f : st.m;
 #pragma unroll
   for (int i = 0; i < NV; ++i) x[i] = fast_exp2(x[i] - m_ref);
-  st.m = m_new;
-  return alpha;
+  return move;
 }
 
 template <int NT, bool TREE>
-__device__ __forceinline__ bool visible(int j, int Lb, int N, const uint64_t (&anc)[NT], int nt) {
+__device__ __forceinline__ bool visible(int j, int Lb, int k_end, int N, const uint64_t (&anc)[NT],
+                                        int nt) {
+  if (j >= k_end) return false;
   if (j < Lb) return true;
   if (!TREE) return false;
   const unsigned m = (unsigned)(j - Lb);
@@ -222,7 +283,8 @@ __device__ __forceinline__ bool visible(int j, int Lb, int N, const uint64_t (&a
 template <int NT, bool TREE>
 __device__ __forceinline__ void step(const Bf16Path::KV& f, const Bf16Path::QFrag (&qf)[NT],
                                      SoftmaxState (&sm)[NT], f32x4_t (&acc)[NT][8], int j0, int Lb,
-                                     int N, const uint64_t (&anc)[NT], float scale_log2, int g) {
+                                     int k_end, int N, const uint64_t (&anc)[NT], float scale_log2,
+                                     int g) {
   f32x4_t s[2][NT];
 #pragma unroll
   for (int kt = 0; kt < 2; ++kt)
@@ -237,18 +299,19 @@ __device__ __forceinline__ void step(const Bf16Path::KV& f, const Bf16Path::QFra
     }
 
   // V^T operands: tile t holds head dim 8*c + t of the 8 keys of this lane's
-  // k-slots, i.e. element t of each loaded 8-dim chunk, two keys per dword.
+  // k-slots, i.e. element t of each loaded 8-dim chunk, two keys per dword
+  // (one byte permute per dword).
   u32x4_t vt[8];
 #pragma unroll
   for (int w = 0; w < 4; ++w)
 #pragma unroll
     for (int e = 0; e < 4; ++e) {
       const uint32_t a = f.v[2 * e][w], b = f.v[2 * e + 1][w];
-      vt[2 * w][e] = (a & 0xFFFFu) | (b << 16);
-      vt[2 * w + 1][e] = (a >> 16) | (b & 0xFFFF0000u);
+      vt[2 * w][e] = __builtin_amdgcn_perm(b, a, 0x05040100u);      // low halves
+      vt[2 * w + 1][e] = __builtin_amdgcn_perm(b, a, 0x07060302u);  // high halves
     }
 
-  const bool need_mask = (j0 + 32 > Lb);
+  const bool need_mask = (j0 + 32 > min(Lb, k_end));
 #pragma unroll
   for (int nt = 0; nt < NT; ++nt) {
     float x[8];
@@ -256,11 +319,15 @@ __device__ __forceinline__ void step(const Bf16Path::KV& f, const Bf16Path::QFra
     for (int kt = 0; kt < 2; ++kt)
 #pragma unroll
       for (int r = 0; r < 4; ++r) {
-        float v = s[kt][nt][r] * scale_log2;
-        if (need_mask && !visible<NT, TREE>(j0 + 16 * kt + 4 * g + r, Lb, N, anc, nt)) v = neg_inf();
+        float v = s[kt][nt][r];
+        if (need_mask && !visible<NT, TREE>(j0 + 16 * kt + 4 * g + r, Lb, k_end, N, anc, nt)) v = neg_inf();
         x[4 * kt + r] = v;
       }
-    const float alpha = softmax_step<8>(x, sm[nt]);
+    float alpha;
+    if (softmax_update<8>(x, sm[nt], scale_log2, alpha)) {
+#pragma unroll
+      for (int t = 0; t < 8; ++t) acc[nt][t] *= alpha;
+    }
     u32x4_t pw;
     float psum = 0.f;
 #pragma unroll
@@ -268,21 +335,20 @@ __device__ __forceinline__ void step(const Bf16Path::KV& f, const Bf16Path::QFra
       pw[e] = pack_bf16x2(x[2 * e], x[2 * e + 1]);
       psum += bf16_lo(pw[e]) + bf16_hi(pw[e]);
     }
-    sm[nt].l = sm[nt].l * alpha + psum;
+    sm[nt].l += psum;
 #pragma unroll
-    for (int t = 0; t < 8; ++t) {
-      acc[nt][t] *= alpha;
+    for (int t = 0; t < 8; ++t)
       acc[nt][t] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(as_bf16x8(vt[t]), as_bf16x8(pw), acc[nt][t],
                                                            0, 0, 0);
-    }
   }
 }
 
 template <int NT, bool TREE>
 __device__ __forceinline__ void step(const F32Path::KV& f, const F32Path::QFrag (&qf)[NT],
                                      SoftmaxState (&sm)[NT], f32x4_t (&acc)[NT][8], int j0, int Lb,
-                                     int N, const uint64_t (&anc)[NT], float scale_log2, int g) {
-  const bool need_mask = (j0 + 16 > Lb);
+                                     int k_end, int N, const uint64_t (&anc)[NT], float scale_log2,
+                                     int g) {
+  const bool need_mask = (j0 + 16 > min(Lb, k_end));
 #pragma unroll
   for (int nt = 0; nt < NT; ++nt) {
     f32x4_t a = {0.f, 0.f, 0.f, 0.f};
@@ -294,14 +360,16 @@ __device__ __forceinline__ void step(const F32Path::KV& f, const F32Path::QFrag 
     float x[4];
 #pragma unroll
     for (int r = 0; r < 4; ++r) {
-      float v = a[r] * scale_log2;
-      if (need_mask && !visible<NT, TREE>(j0 + 4 * g + r, Lb, N, anc, nt)) v = neg_inf();
+      float v = a[r];
+      if (need_mask && !visible<NT, TREE>(j0 + 4 * g + r, Lb, k_end, N, anc, nt)) v = neg_inf();
       x[r] = v;
     }
-    const float alpha = softmax_step<4>(x, sm[nt]);
-    sm[nt].l = sm[nt].l * alpha + ((x[0] + x[1]) + (x[2] + x[3]));
+    float alpha;
+    if (softmax_update<4>(x, sm[nt], scale_log2, alpha)) {
 #pragma unroll
-    for (int t = 0; t < 8; ++t) acc[nt][t] *= alpha;
+      for (int t = 0; t < 8; ++t) acc[nt][t] *= alpha;
+    }
+    sm[nt].l += (x[0] + x[1]) + (x[2] + x[3]);
 #pragma unroll
     for (int r = 0; r < 4; ++r)
 #pragma unroll
@@ -325,21 +393,39 @@ __device__ __forceinline__ void store_row8(float* dst, const float (&o)[8]) {
   *(f32x4_t*)(dst + 4) = f32x4_t{o[4], o[5], o[6], o[7]};
 }
 
-__device__ __forceinline__ void store_4(uint16_t* dst, f32x4_t o) {
-  uint32_t w0 = pack_bf16x2(o[0], o[1]), w1 = pack_bf16x2(o[2], o[3]);
-  *(uint2*)dst = make_uint2(w0, w1);
+__device__ __forceinline__ void store_2(uint16_t* dst, float a, float b) {
+  *(uint32_t*)dst = pack_bf16x2(a, b);
 }
 
-__device__ __forceinline__ void store_4(float* dst, f32x4_t o) { *(f32x4_t*)dst = o; }
+__device__ __forceinline__ void store_2(float* dst, float a, float b) { *(float2*)dst = make_float2(a, b); }
 
-template <class P, int NT, bool TREE>
+// Work of one wave: the query tiles it owns and the key steps it takes.
+// QG query groups split the 16-row query tiles; the 4 / QG waves of a group
+// interleave the key steps of the split, so each K/V step is loaded by one
+// wave per group (QG = 2 loads it twice, the second time from L2).
+template <class P, int NT, int QG, bool TREE>
+struct WaveTask {
+  static constexpr int kWavesPerGroup = kWaves / QG;
+  static constexpr int kStride = P::kStep * kWavesPerGroup;
+  // K/V steps in flight per wave: three for one query tile, two when the
+  // accumulators of two tiles need the registers.
+  static constexpr int kBufs = NT == 1 ? 3 : 2;
+};
+
+template <class P, int NT, int QG, bool TREE>
 __global__ __launch_bounds__(kThreads) void tree_attn_kernel(AttnArgs args) {
   typedef typename P::elem_t elem_t;
+  typedef WaveTask<P, NT, QG, TREE> Task;
   constexpr int kStep = P::kStep;
+  constexpr int kBufs = Task::kBufs;
+  constexpr int kWpg = Task::kWavesPerGroup;
+  constexpr int kStride = Task::kStride;
 
   const int s = blockIdx.x, h = blockIdx.y, b = blockIdx.z;
-  const int tid = threadIdx.x, wave = tid >> 6, lane = tid & 63;
+  const int tid = threadIdx.x, lane = tid & 63;
+  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
   const int c = lane & 15, g = lane >> 4;
+  const int qg = wave / kWpg, wig = wave % kWpg;  // query group, wave in group
   const int N = args.N, H = args.H, Lcap = args.L_cap;
 
   const int Lb = min(max(args.seq_lens[b], 0), TREE ? Lcap - N : Lcap);
@@ -348,25 +434,39 @@ __global__ __launch_bounds__(kThreads) void tree_attn_kernel(AttnArgs args) {
   if (s >= nsplit) return;
   const int k_begin = s * args.chunk;
   const int k_end = min(T, k_begin + args.chunk);
-  const int kmax = max(T - 1, 0);
 
   const size_t head_off = ((size_t)b * H + h) * (size_t)Lcap * kD;
-  const elem_t* kp = (const elem_t*)args.k + head_off;
-  const elem_t* vp = (const elem_t*)args.v + head_off;
+  const char* kslab = (const char*)((const elem_t*)args.k + head_off);
+  const char* vslab = (const char*)((const elem_t*)args.v + head_off);
   const elem_t* qp = (const elem_t*)args.q;
+  const LaneOffsets lo = lane_offsets(P{}, c, g);
 
+  // Small loads first, then the first kBufs K/V steps, so that the K/V
+  // requests are in flight while the ancestor masks are built and the loop
+  // is entered with exactly its buffers' loads outstanding, in order.
+  int my_parent = -1;
+  if (TREE && lane < N) my_parent = args.parents[(size_t)b * N + lane];
   typename P::QFrag qf[NT];
 #pragma unroll
   for (int nt = 0; nt < NT; ++nt) {
-    const int n = 16 * nt + c;
+    const int n = 16 * (qg * NT + nt) + c;
     load_q<P>(qf[nt], qp + (((size_t)b * N + min(n, N - 1)) * H + h) * kD, n < N, g);
   }
+  __builtin_amdgcn_sched_barrier(0);
+
+  // This wave's key steps: [first + i * kStride, + kStep), i < nsteps.
+  const int first = k_begin + kStep * wig;
+  const int nsteps = first < k_end ? (k_end - first + kStride - 1) / kStride : 0;
+  typename P::KV buf[kBufs];
+#pragma unroll
+  for (int u = 0; u < kBufs; ++u) load_kv(buf[u], kslab, vslab, first + u * kStride, k_end, lo);
+  __builtin_amdgcn_sched_barrier(0);
 
   uint64_t anc[NT];
   if (TREE) {
-    const uint64_t mine = ancestor_mask(args.parents + (size_t)b * N, N, lane);
+    const uint64_t mine = ancestor_mask_from(my_parent, N, lane);
 #pragma unroll
-    for (int nt = 0; nt < NT; ++nt) anc[nt] = shfl_u64(mine, min(16 * nt + c, 63));
+    for (int nt = 0; nt < NT; ++nt) anc[nt] = shfl_u64(mine, min(16 * (qg * NT + nt) + c, 63));
   } else {
 #pragma unroll
     for (int nt = 0; nt < NT; ++nt) anc[nt] = 0;
@@ -382,130 +482,150 @@ __global__ __launch_bounds__(kThreads) void tree_attn_kernel(AttnArgs args) {
     for (int t = 0; t < 8; ++t) acc[nt][t] = f32x4_t{0.f, 0.f, 0.f, 0.f};
   }
 
-  // Main loop: each wave takes every kWaves-th step of the split; the next
-  // step's K/V are requested before the current one is consumed.
-  int j0 = k_begin + kStep * wave;
-  if (j0 < k_end) {
-    typename P::KV cur, nxt;
-    load_kv(cur, kp, vp, j0, kmax, c, g);
-    for (;;) {
-      const int jn = j0 + kStep * kWaves;
-      const bool more = jn < k_end;
-      if (more) load_kv(nxt, kp, vp, jn, kmax, c, g);
-      step<NT, TREE>(cur, qf, sm, acc, j0, Lb, N, anc, args.scale_log2, g);
-      if (!more) break;
-      cur = nxt;
-      j0 = jn;
+  // Main loop, unrolled over the buffers: consume buffer u, refill it with
+  // the step kBufs ahead.  The trip count is rounded up to whole rounds of
+  // kBufs steps so the body is straight-line code and every wait leaves the
+  // other buffers' loads in flight; steps at or past k_end read zeros and
+  // are fully masked.
+  const int iters = (nsteps + kBufs - 1) / kBufs;
+  int j = first;
+  for (int it = 0; it < iters; ++it) {
+#pragma unroll
+    for (int u = 0; u < kBufs; ++u) {
+      step<NT, TREE>(buf[u], qf, sm, acc, j, Lb, k_end, N, anc, args.scale_log2, g);
+      load_kv(buf[u], kslab, vslab, j + kBufs * kStride, k_end, lo);
+      j += kStride;
     }
   }
 
 #pragma unroll
   for (int nt = 0; nt < NT; ++nt) sm[nt].l = sum_across_groups(sm[nt].l);
 
-  // Merge the four waves' states through LDS (lane-major: conflict free).
-  __shared__ float lds_o[(kWaves - 1) * NT * 8 * 4 * 64];
-  __shared__ float lds_m[(kWaves - 1) * NT * 64];
-  __shared__ float lds_l[(kWaves - 1) * NT * 64];
-  __shared__ int lds_last;
-  if (wave > 0) {
-    const int w = wave - 1;
+  // Merge the waves of each query group through LDS (lane-major stores and
+  // loads: conflict free).  Wave 0 of each group finishes the group's tiles.
+  constexpr int kSlots = QG * (kWpg - 1) * NT;
+  __shared__ float lds_o[kSlots * 8 * 4 * 64];
+  __shared__ float lds_m[kSlots * 64];
+  __shared__ float lds_l[kSlots * 64];
+  if (wig > 0) {
 #pragma unroll
     for (int nt = 0; nt < NT; ++nt) {
-      lds_m[(w * NT + nt) * 64 + lane] = sm[nt].m;
-      lds_l[(w * NT + nt) * 64 + lane] = sm[nt].l;
+      const int slot = (qg * (kWpg - 1) + wig - 1) * NT + nt;
+      lds_m[slot * 64 + lane] = sm[nt].m;
+      lds_l[slot * 64 + lane] = sm[nt].l;
 #pragma unroll
       for (int t = 0; t < 8; ++t)
 #pragma unroll
-        for (int r = 0; r < 4; ++r) lds_o[(((w * NT + nt) * 8 + t) * 4 + r) * 64 + lane] = acc[nt][t][r];
+        for (int r = 0; r < 4; ++r) lds_o[((slot * 8 + t) * 4 + r) * 64 + lane] = acc[nt][t][r];
     }
   }
   __syncthreads();
+  if (wig != 0) return;
 
-  if (wave == 0) {
-    const size_t part_base = (((size_t)b * H + h) * args.splits + s) * N;
+  const size_t part_base = (((size_t)b * H + h) * args.splits + s) * N;
 #pragma unroll
-    for (int nt = 0; nt < NT; ++nt) {
-      float mw[kWaves], fw[kWaves];
-      mw[0] = sm[nt].m;
+  for (int nt = 0; nt < NT; ++nt) {
+    float mw[kWpg], fw[kWpg];
+    mw[0] = sm[nt].m;
 #pragma unroll
-      for (int w = 1; w < kWaves; ++w) mw[w] = lds_m[((w - 1) * NT + nt) * 64 + lane];
-      float M = mw[0];
+    for (int w = 1; w < kWpg; ++w) mw[w] = lds_m[((qg * (kWpg - 1) + w - 1) * NT + nt) * 64 + lane];
+    float M = mw[0];
 #pragma unroll
-      for (int w = 1; w < kWaves; ++w) M = fmaxf(M, mw[w]);
+    for (int w = 1; w < kWpg; ++w) M = fmaxf(M, mw[w]);
 #pragma unroll
-      for (int w = 0; w < kWaves; ++w) fw[w] = (M == neg_inf()) ? 0.f : fast_exp2(mw[w] - M);
-      float L = fw[0] * sm[nt].l;
+    for (int w = 0; w < kWpg; ++w) fw[w] = (M == neg_inf()) ? 0.f : fast_exp2(mw[w] - M);
+    float L = fw[0] * sm[nt].l;
 #pragma unroll
-      for (int w = 1; w < kWaves; ++w) L += fw[w] * lds_l[((w - 1) * NT + nt) * 64 + lane];
+    for (int w = 1; w < kWpg; ++w) L += fw[w] * lds_l[((qg * (kWpg - 1) + w - 1) * NT + nt) * 64 + lane];
 
-      const int n = 16 * nt + c;
-      const float inv = (nsplit == 1) ? ((L > 0.f) ? 1.f / L : 0.f) : 1.f;
+    const int n = 16 * (qg * NT + nt) + c;
+    const float inv = (nsplit == 1) ? ((L > 0.f) ? 1.f / L : 0.f) : 1.f;
 #pragma unroll
-      for (int r = 0; r < 4; ++r) {
-        float o[8];
+    for (int r = 0; r < 4; ++r) {
+      float o[8];
 #pragma unroll
-        for (int t = 0; t < 8; ++t) {
-          float v = fw[0] * acc[nt][t][r];
+      for (int t = 0; t < 8; ++t) {
+        float v = fw[0] * acc[nt][t][r];
 #pragma unroll
-          for (int w = 1; w < kWaves; ++w) v += fw[w] * lds_o[((((w - 1) * NT + nt) * 8 + t) * 4 + r) * 64 + lane];
-          o[t] = v * inv;
-        }
-        if (n < N) {
-          const int d = 32 * g + 8 * r;
-          if (nsplit == 1)
-            store_row8((elem_t*)args.out + (((size_t)b * N + n) * H + h) * kD + d, o);
-          else
-            store_row8(args.part_o + (part_base + n) * kD + d, o);
-        }
+        for (int w = 1; w < kWpg; ++w)
+          v += fw[w] * lds_o[((((qg * (kWpg - 1) + w - 1) * NT + nt) * 8 + t) * 4 + r) * 64 + lane];
+        o[t] = v * inv;
       }
-      if (nsplit > 1 && n < N && g == 0) args.part_ml[part_base + n] = make_float2(M, L);
+      if (n < N) {
+        const int d = 32 * g + 8 * r;
+        if (nsplit == 1)
+          store_row8((elem_t*)args.out + (((size_t)b * N + n) * H + h) * kD + d, o);
+        else
+          store_row8(args.part_o + (part_base + n) * kD + d, o);
+      }
+    }
+    if (nsplit > 1 && n < N && g == 0) args.part_ml[part_base + n] = make_float2(M, L);
+  }
+}
+
+// Merges the split partial states of every (sequence, head) whose keys were
+// divided, in a fixed split order (the result does not depend on timing).
+// One wave per output row (sequence, query, head); each lane owns two head
+// dims and requests kBatch splits' partials at a time.
+constexpr int kCombineRows = kWaves;  // rows per workgroup
+
+template <class P>
+__global__ __launch_bounds__(kThreads) void tree_attn_combine(AttnArgs args) {
+  typedef typename P::elem_t elem_t;
+  constexpr int kBatch = 8;
+  const int N = args.N, H = args.H, Lcap = args.L_cap;
+  const int row = blockIdx.x * kCombineRows + (threadIdx.x >> 6);  // (b, n, h) in out order
+  const int lane = threadIdx.x & 63;
+  if (row >= args.B * N * H) return;
+  const int h = row % H, n = (row / H) % N, b = row / (H * N);
+  const bool tree = args.parents != nullptr;
+  const int Lb = min(max(args.seq_lens[b], 0), tree ? Lcap - N : Lcap);
+  const int T = Lb + (tree ? N : 0);
+  const int nsplit = max(1, (T + args.chunk - 1) / args.chunk);
+  if (nsplit == 1) return;  // written directly by the attention kernel
+  const size_t base = ((size_t)b * H + h) * args.splits * N + n;  // + sp * N
+  float M = neg_inf(), L = 0.f, o0 = 0.f, o1 = 0.f;
+  for (int s0 = 0; s0 < nsplit; s0 += kBatch) {
+    // Request a batch of splits at once; entries past nsplit get max -inf
+    // (weight 0), so the merge below has no branches to sink the loads into.
+    float2 ml[kBatch], ov[kBatch];
+#pragma unroll
+    for (int u = 0; u < kBatch; ++u) {
+      const int sp = min(s0 + u, nsplit - 1);
+      ml[u] = args.part_ml[base + (size_t)sp * N];
+      ov[u] = *(const float2*)(args.part_o + (base + (size_t)sp * N) * kD + 2 * lane);
+    }
+#pragma unroll
+    for (int u = 0; u < kBatch; ++u) {
+      const float mu = (s0 + u < nsplit) ? ml[u].x : neg_inf();
+      const float m_new = fmaxf(M, mu);
+      const float a = (m_new == neg_inf()) ? 0.f : fast_exp2(M - m_new);
+      const float f = (m_new == neg_inf()) ? 0.f : fast_exp2(mu - m_new);
+      L = L * a + f * ml[u].y;
+      o0 = o0 * a + f * ov[u].x;
+      o1 = o1 * a + f * ov[u].y;
+      M = m_new;
     }
   }
-  if (nsplit == 1) return;
-
-  // Publish this split's partial state; the last split of (b, h) merges.
-  __threadfence();
-  __syncthreads();
-  if (tid == 0) {
-    const uint32_t prev = __hip_atomic_fetch_add(args.counters + (size_t)b * H + h, 1u,
-                                                 __ATOMIC_ACQ_REL, __HIP_MEMORY_SCOPE_AGENT);
-    lds_last = (prev == (uint32_t)(nsplit - 1));
-  }
-  __syncthreads();
-  if (!lds_last) return;
-  __threadfence();
-
-  const size_t bh_base = ((size_t)b * H + h) * args.splits;
-  for (int item = tid; item < N * (kD / 4); item += kThreads) {
-    const int n = item / (kD / 4), dq = item % (kD / 4);
-    float M = neg_inf();
-    for (int sp = 0; sp < nsplit; ++sp) M = fmaxf(M, args.part_ml[(bh_base + sp) * N + n].x);
-    float L = 0.f;
-    f32x4_t o = {0.f, 0.f, 0.f, 0.f};
-    for (int sp = 0; sp < nsplit; ++sp) {
-      const float2 ml = args.part_ml[(bh_base + sp) * N + n];
-      const float f = (M == neg_inf()) ? 0.f : fast_exp2(ml.x - M);
-      L += f * ml.y;
-      o += f * *(const f32x4_t*)(args.part_o + ((bh_base + sp) * N + n) * kD + 4 * dq);
-    }
-    const float inv = (L > 0.f) ? 1.f / L : 0.f;
-    store_4((elem_t*)args.out + (((size_t)b * N + n) * H + h) * kD + 4 * dq, o * inv);
-  }
-  if (tid == 0)
-    __hip_atomic_store(args.counters + (size_t)b * H + h, 0u, __ATOMIC_RELAXED,
-                       __HIP_MEMORY_SCOPE_AGENT);
+  const float inv = (L > 0.f) ? 1.f / L : 0.f;
+  store_2((elem_t*)args.out + (size_t)row * kD + 2 * lane, o0 * inv, o1 * inv);
 }
 
 template <class P, bool TREE>
 hipError_t launch_nt(const AttnArgs& a, hipStream_t stream) {
   const dim3 grid(a.splits, a.H, a.B), block(kThreads);
-  const int nt = (a.N + 15) / 16;
-  switch (nt) {
-    case 1: hipLaunchKernelGGL((tree_attn_kernel<P, 1, TREE>), grid, block, 0, stream, a); break;
-    case 2: hipLaunchKernelGGL((tree_attn_kernel<P, 2, TREE>), grid, block, 0, stream, a); break;
-    case 3: hipLaunchKernelGGL((tree_attn_kernel<P, 3, TREE>), grid, block, 0, stream, a); break;
-    default: hipLaunchKernelGGL((tree_attn_kernel<P, 4, TREE>), grid, block, 0, stream, a); break;
-  }
+  const int tiles = (a.N + 15) / 16;
+  if (tiles == 1)
+    hipLaunchKernelGGL((tree_attn_kernel<P, 1, 1, TREE>), grid, block, 0, stream, a);
+  else if (tiles == 2)
+    hipLaunchKernelGGL((tree_attn_kernel<P, 2, 1, TREE>), grid, block, 0, stream, a);
+  else
+    hipLaunchKernelGGL((tree_attn_kernel<P, 2, 2, TREE>), grid, block, 0, stream, a);
+  hipError_t e = hipGetLastError();
+  if (e != hipSuccess || a.splits == 1) return e;
+  const int rows = a.B * a.N * a.H;
+  hipLaunchKernelGGL((tree_attn_combine<P>), dim3((rows + kCombineRows - 1) / kCombineRows), block, 0,
+                     stream, a);
   return hipGetLastError();
 }
 
@@ -514,13 +634,15 @@ hipError_t launch_nt(const AttnArgs& a, hipStream_t stream) {
 AttnPlan plan_tree_attn(int B, int N, int H, int L_cap, int max_splits) {
   AttnPlan p{};
   const int keys = L_cap;  // upper bound on the keys any query sees
+  const long bh = (long)B * H;
   int want;
   if (max_splits > 0) {
     want = max_splits;
   } else {
-    const long bh = (long)B * H;
-    want = (int)((2L * kNumCU + bh - 1) / bh);          // about two workgroups per CU
-    want = min(want, (keys + 255) / 256);               // at least ~256 keys each
+    // One 4-wave workgroup fills a CU; split until the grid covers the CUs
+    // once, keeping at least kMinChunk keys per split.
+    want = (int)(kNumCU / bh);
+    want = min(want, (keys + kMinChunk - 1) / kMinChunk);
   }
   want = max(1, min(want, kMaxSplits));
   int chunk = (keys + want - 1) / want;
@@ -531,11 +653,10 @@ AttnPlan plan_tree_attn(int B, int N, int H, int L_cap, int max_splits) {
     p.ws_bytes = 0;
     return p;
   }
-  const size_t units = (size_t)B * H * p.splits * N;
-  p.part_o_off = 0;
-  p.part_ml_off = ((units * kHeadDim * sizeof(float)) + 255) & ~(size_t)255;
-  p.counter_off = (p.part_ml_off + units * sizeof(float2) + 255) & ~(size_t)255;
-  p.ws_bytes = p.counter_off + (size_t)B * H * sizeof(uint32_t);
+  const size_t units = (size_t)bh * p.splits * N;
+  p.part_ml_off = 0;
+  p.part_o_off = (units * sizeof(float2) + 255) & ~(size_t)255;
+  p.ws_bytes = p.part_o_off + units * kHeadDim * sizeof(float);
   return p;
 }
 

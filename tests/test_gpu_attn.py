@@ -49,7 +49,7 @@ def run_case(B, N, H, lens, kind, dtype, splits, seed, l_cap=None):
     v = cpu_normal((B, H, L_cap, D), seed + 2, dtype)
     parents = _parents(kind, B, N, seed)
     dev = torch.device("cuda")
-    out = torch.empty((B, N, H, D), dtype=dtype, device=dev)
+    out = torch.full((B, N, H, D), float("nan"), dtype=dtype, device=dev)
     glide.glide_tree_attn(q.to(dev), k.to(dev), v.to(dev),
                           torch.tensor(lens, dtype=torch.int32, device=dev),
                           None if parents is None else torch.from_numpy(parents).to(dev),
@@ -134,6 +134,36 @@ def test_deterministic_and_split_invariant():
     base = outs[1][0].float()
     for s, os_ in outs.items():
         assert float((os_[0].float() - base).abs().max()) <= BF16_TOL
+
+
+def test_workspace_reused_across_shapes():
+    """One workspace serves calls of different shapes in turn (each call
+    writes the partial states it reads)."""
+    require_gpu()
+    dev = torch.device("cuda")
+    big = glide.attn_workspace(4, 64, 8, 4160, 0, dev)
+    ws = torch.full((big.numel(),), 0xFF, dtype=torch.uint8, device=dev)  # garbage on purpose
+    shapes = [(4, 64, 8, 4096, 0), (1, 16, 2, 2048, 9), (2, 5, 3, 1000, 3), (4, 64, 8, 4096, 0),
+              (1, 16, 2, 2048, 64)]
+    for i, (B, N, H, L, splits) in enumerate(shapes):
+        say("ws reuse", B, N, H, L, splits)
+        q = cpu_normal((B, N, H, D), 40 + i, torch.bfloat16)
+        k = cpu_normal((B, H, L + N, D), 50 + i, torch.bfloat16)
+        v = cpu_normal((B, H, L + N, D), 60 + i, torch.bfloat16)
+        par = W.random_parents(B, N, 6, i)
+        out = torch.full((B, N, H, D), float("nan"), dtype=torch.bfloat16, device=dev)
+        lens = [L - 37 * b for b in range(B)]
+        glide.glide_tree_attn(q.to(dev), k.to(dev), v.to(dev),
+                              torch.tensor(lens, dtype=torch.int32, device=dev),
+                              torch.from_numpy(par).to(dev), out, max_splits=splits, workspace=ws)
+        torch.cuda.synchronize()
+        got = to64(out)
+        # sample two heads per shape against the oracle
+        for b in range(B):
+            for h in (0, H - 1):
+                ref = OA.tree_attention_head(to64(q[b, :, h]), to64(k[b, h]), to64(v[b, h]),
+                                             lens[b], par[b])
+                assert float(np.abs(got[b, :, h] - ref).max()) <= BF16_TOL
 
 
 def test_validation_reports_bad_device_data(monkeypatch):
