@@ -91,7 +91,7 @@ class Step:
         self.ws = glide.attn_workspace(B, N, wl.heads, L_cap, max_splits, dev)
         self.xws = (glide.attn_workspace(B, wl.depth, wl.heads, L_cap, max_splits, dev)
                     if wl.cross else None)
-        self.cape_ws = torch.empty(max(glide.load().cape_expand_workspace(B, wl.depth), 1),
+        self.cape_ws = torch.empty(max(glide.load().cape_expand_workspace(B, wl.depth, V), 1),
                                    dtype=torch.uint8, device=dev)
         elem = 2 if dtype == torch.bfloat16 else 4
         self.verify_bytes = attn_bytes(self.lens_np, N, wl.heads, elem, True)

@@ -117,8 +117,9 @@ int glide_tree_attn(const void* q, const void* k_cache, const void* v_cache,
                     int dtype, float scale, int max_splits,
                     void* workspace, size_t ws_bytes, hipStream_t stream);
 
-/* Workspace bytes cape_expand needs (the per-row top candidates). */
-size_t cape_expand_workspace(int B, int gamma);
+/* Workspace bytes cape_expand needs (the best candidates of every 4096-token
+ * part of every draft row); 0 for invalid sizes. */
+size_t cape_expand_workspace(int B, int gamma, int V);
 
 /*
  * cape_expand -- confidence-aware proposal expansion (Sec. 4.2).
@@ -140,7 +141,7 @@ size_t cape_expand_workspace(int B, int gamma);
  *   draft_probs [B, gamma, V] float32, finite (no NaN).
  *   tokens_out, parents_out [B, n_max] int32; n_nodes_out [B] int32.
  *   B >= 1; 1 <= gamma <= n_max <= 64; V >= 2; 0 <= k (<= 7 when fixed).
- *   workspace >= cape_expand_workspace(B, gamma) bytes (no zero-fill needed).
+ *   workspace >= cape_expand_workspace(B, gamma, V) bytes (no zero-fill needed).
  */
 int cape_expand(const float* draft_probs, int B, int gamma, int V, int k,
                 int fixed, int n_max, int32_t* tokens_out,

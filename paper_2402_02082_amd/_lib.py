@@ -49,7 +49,7 @@ def load():
     lib.glide_tree_attn.restype = I
     lib.glide_tree_attn.argtypes = [P, P, P, P, P, P, I, I, I, I, I, I, F, I, P, Z, P]
     lib.cape_expand_workspace.restype = Z
-    lib.cape_expand_workspace.argtypes = [I, I]
+    lib.cape_expand_workspace.argtypes = [I, I, I]
     lib.cape_expand.restype = I
     lib.cape_expand.argtypes = [P, I, I, I, I, I, I, P, P, P, P, Z, P]
     lib.glide_argmax_rows.restype = I
@@ -152,7 +152,7 @@ def cape_expand(draft_probs, k, n_max, tokens_out, parents_out, n_nodes_out, fix
                            ("n_nodes_out", n_nodes_out, (B,))):
         _dev(t, name, torch.int32)
         _need(tuple(t.shape) == shape, "%s must be %s" % (name, shape))
-    need = load().cape_expand_workspace(B, gamma)
+    need = load().cape_expand_workspace(B, gamma, V)
     if workspace is None:
         workspace = torch.empty(max(need, 1), dtype=torch.uint8, device=draft_probs.device)
     status = load().cape_expand(

@@ -125,9 +125,9 @@ int glide_tree_attn(const void* q, const void* k_cache, const void* v_cache, con
   return hip_status(glide::launch_tree_attn(a, dtype == GLIDE_BF16, stream));
 }
 
-size_t cape_expand_workspace(int B, int gamma) {
-  if (B < 1 || gamma < 1 || gamma > glide::kMaxNodes) return 0;
-  return glide::cape_workspace_bytes(B, gamma);
+size_t cape_expand_workspace(int B, int gamma, int V) {
+  if (B < 1 || gamma < 1 || gamma > glide::kMaxNodes || V < 2) return 0;
+  return glide::cape_workspace_bytes(B, gamma, V);
 }
 
 int cape_expand(const float* draft_probs, int B, int gamma, int V, int k, int fixed, int n_max,
@@ -137,7 +137,7 @@ int cape_expand(const float* draft_probs, int B, int gamma, int V, int k, int fi
   if (B < 1 || gamma < 1 || n_max < gamma || n_max > glide::kMaxNodes || V < 2) return GLIDE_EINVAL;
   if (k < 0 || (fixed && k > GLIDE_CAPE_MAX_K)) return GLIDE_EINVAL;
   if ((double)B * gamma * V > 9.0e18) return GLIDE_EINVAL;
-  if (ws_bytes < glide::cape_workspace_bytes(B, gamma)) return GLIDE_EINVAL;
+  if (ws_bytes < glide::cape_workspace_bytes(B, gamma, V)) return GLIDE_EINVAL;
   return hip_status(glide::launch_cape_expand(draft_probs, B, gamma, V, k, fixed ? 1 : 0, n_max,
                                               tokens_out, parents_out, n_nodes_out, workspace,
                                               stream));

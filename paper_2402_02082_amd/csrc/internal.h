@@ -39,7 +39,7 @@ struct AttnArgs {
 
 hipError_t launch_tree_attn(const AttnArgs& a, bool bf16, hipStream_t stream);
 
-size_t cape_workspace_bytes(int B, int gamma);
+size_t cape_workspace_bytes(int B, int gamma, int V);
 hipError_t launch_cape_expand(const float* probs, int B, int gamma, int V, int k,
                               int fixed, int n_max, int32_t* tokens,
                               int32_t* parents, int32_t* n_nodes, void* ws,

@@ -428,22 +428,17 @@ __global__ __launch_bounds__(kThreads) void tree_attn_kernel(AttnArgs args) {
   const int qg = wave / kWpg, wig = wave % kWpg;  // query group, wave in group
   const int N = args.N, H = args.H, Lcap = args.L_cap;
 
-  const int Lb = min(max(args.seq_lens[b], 0), TREE ? Lcap - N : Lcap);
-  const int T = Lb + (TREE ? N : 0);  // keys visible to some query
-  const int nsplit = max(1, (T + args.chunk - 1) / args.chunk);
-  if (s >= nsplit) return;
-  const int k_begin = s * args.chunk;
-  const int k_end = min(T, k_begin + args.chunk);
-
   const size_t head_off = ((size_t)b * H + h) * (size_t)Lcap * kD;
   const char* kslab = (const char*)((const elem_t*)args.k + head_off);
   const char* vslab = (const char*)((const elem_t*)args.v + head_off);
   const elem_t* qp = (const elem_t*)args.q;
   const LaneOffsets lo = lane_offsets(P{}, c, g);
 
-  // Small loads first, then the first kBufs K/V steps, so that the K/V
-  // requests are in flight while the ancestor masks are built and the loop
-  // is entered with exactly its buffers' loads outstanding, in order.
+  // Everything that does not depend on the sequence length is requested at
+  // once: the length itself, the parent links, the queries and -- assuming
+  // the split is full -- the first kBufs K/V steps (rows below L_cap, so in
+  // bounds).  The length only arrives with them, one round trip later.
+  const int raw_len = args.seq_lens[b];
   int my_parent = -1;
   if (TREE && lane < N) my_parent = args.parents[(size_t)b * N + lane];
   typename P::QFrag qf[NT];
@@ -452,24 +447,35 @@ __global__ __launch_bounds__(kThreads) void tree_attn_kernel(AttnArgs args) {
     const int n = 16 * (qg * NT + nt) + c;
     load_q<P>(qf[nt], qp + (((size_t)b * N + min(n, N - 1)) * H + h) * kD, n < N, g);
   }
-  __builtin_amdgcn_sched_barrier(0);
-
-  // This wave's key steps: [first + i * kStride, + kStep), i < nsteps.
-  const int first = k_begin + kStep * wig;
-  const int nsteps = first < k_end ? (k_end - first + kStride - 1) / kStride : 0;
+  const int k_begin = s * args.chunk;
+  const int first = k_begin + kStep * wig;  // this wave's steps: first + i * kStride
+  const int full_end = min(Lcap, k_begin + args.chunk);
   typename P::KV buf[kBufs];
 #pragma unroll
-  for (int u = 0; u < kBufs; ++u) load_kv(buf[u], kslab, vslab, first + u * kStride, k_end, lo);
+  for (int u = 0; u < kBufs; ++u) load_kv(buf[u], kslab, vslab, first + u * kStride, full_end, lo);
   __builtin_amdgcn_sched_barrier(0);
 
+  const int Lb = min(max(raw_len, 0), TREE ? Lcap - N : Lcap);
+  const int T = Lb + (TREE ? N : 0);  // keys visible to some query
+  const int nsplit = max(1, (T + args.chunk - 1) / args.chunk);
+  if (s >= nsplit) return;
+  const int k_end = min(T, k_begin + args.chunk);
+  const int nsteps = first < k_end ? (k_end - first + kStride - 1) / kStride : 0;
+  if (k_end < full_end) {
+    // The split ends inside the cache: fetch again so that rows past the
+    // sequence (possibly never written) read as zeros.
+#pragma unroll
+    for (int u = 0; u < kBufs; ++u) load_kv(buf[u], kslab, vslab, first + u * kStride, k_end, lo);
+  }
+
+  // Ancestor masks are only needed by the split that holds the tree rows.
   uint64_t anc[NT];
-  if (TREE) {
+#pragma unroll
+  for (int nt = 0; nt < NT; ++nt) anc[nt] = 0;
+  if (TREE && k_end > Lb) {
     const uint64_t mine = ancestor_mask_from(my_parent, N, lane);
 #pragma unroll
     for (int nt = 0; nt < NT; ++nt) anc[nt] = shfl_u64(mine, min(16 * (qg * NT + nt) + c, 63));
-  } else {
-#pragma unroll
-    for (int nt = 0; nt < NT; ++nt) anc[nt] = 0;
   }
 
   SoftmaxState sm[NT];
@@ -579,32 +585,43 @@ __global__ __launch_bounds__(kThreads) void tree_attn_combine(AttnArgs args) {
   if (row >= args.B * N * H) return;
   const int h = row % H, n = (row / H) % N, b = row / (H * N);
   const bool tree = args.parents != nullptr;
-  const int Lb = min(max(args.seq_lens[b], 0), tree ? Lcap - N : Lcap);
+  const size_t base = ((size_t)b * H + h) * args.splits * N + n;  // + sp * N
+  // The sequence length and the first batch of partials are requested
+  // together; partials past this sequence's split count get weight 0.
+  const int raw_len = args.seq_lens[b];
+  float2 ml[kBatch], ov[kBatch];
+#pragma unroll
+  for (int u = 0; u < kBatch; ++u) {
+    const int sp = min(u, args.splits - 1);
+    ml[u] = args.part_ml[base + (size_t)sp * N];
+    ov[u] = *(const float2*)(args.part_o + (base + (size_t)sp * N) * kD + 2 * lane);
+  }
+  const int Lb = min(max(raw_len, 0), tree ? Lcap - N : Lcap);
   const int T = Lb + (tree ? N : 0);
   const int nsplit = max(1, (T + args.chunk - 1) / args.chunk);
   if (nsplit == 1) return;  // written directly by the attention kernel
-  const size_t base = ((size_t)b * H + h) * args.splits * N + n;  // + sp * N
   float M = neg_inf(), L = 0.f, o0 = 0.f, o1 = 0.f;
-  for (int s0 = 0; s0 < nsplit; s0 += kBatch) {
-    // Request a batch of splits at once; entries past nsplit get max -inf
-    // (weight 0), so the merge below has no branches to sink the loads into.
-    float2 ml[kBatch], ov[kBatch];
+  for (int s0 = 0;;) {
+#pragma unroll
+    for (int u = 0; u < kBatch; ++u) {
+      const bool valid = s0 + u < nsplit;
+      const float mu = valid ? ml[u].x : neg_inf();
+      const float m_new = fmaxf(M, mu);
+      const float a = (m_new == neg_inf()) ? 0.f : fast_exp2(M - m_new);
+      const float f = (m_new == neg_inf()) ? 0.f : fast_exp2(mu - m_new);
+      // select, not multiply: entries past nsplit may hold stale values
+      L = L * a + (valid ? f * ml[u].y : 0.f);
+      o0 = o0 * a + (valid ? f * ov[u].x : 0.f);
+      o1 = o1 * a + (valid ? f * ov[u].y : 0.f);
+      M = m_new;
+    }
+    s0 += kBatch;
+    if (s0 >= nsplit) break;
 #pragma unroll
     for (int u = 0; u < kBatch; ++u) {
       const int sp = min(s0 + u, nsplit - 1);
       ml[u] = args.part_ml[base + (size_t)sp * N];
       ov[u] = *(const float2*)(args.part_o + (base + (size_t)sp * N) * kD + 2 * lane);
-    }
-#pragma unroll
-    for (int u = 0; u < kBatch; ++u) {
-      const float mu = (s0 + u < nsplit) ? ml[u].x : neg_inf();
-      const float m_new = fmaxf(M, mu);
-      const float a = (m_new == neg_inf()) ? 0.f : fast_exp2(M - m_new);
-      const float f = (m_new == neg_inf()) ? 0.f : fast_exp2(mu - m_new);
-      L = L * a + f * ml[u].y;
-      o0 = o0 * a + f * ov[u].x;
-      o1 = o1 * a + f * ov[u].y;
-      M = m_new;
     }
   }
   const float inv = (L > 0.f) ? 1.f / L : 0.f;

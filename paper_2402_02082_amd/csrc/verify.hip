@@ -3,8 +3,9 @@
 // when it equals the target's greedy token; Sec. 4.2 verifies the whole
 // expanded proposal in one pass; Sec. 5.1 uses greedy acceptance for CaPE).
 //
-//   argmax_rows   one workgroup per logits row: the first index of the row
-//                 maximum (a max over (order-preserving value, ~index) keys).
+//   argmax_rows   one 1024-thread workgroup per logits row: the first index
+//                 of the row maximum (a max over (order-preserving value,
+//                 ~index) keys).
 //   tree_verify   one wave per sequence, one lane per node: a node is
 //                 accepted iff every node on its root path matches, i.e. its
 //                 ancestor-or-self bitmask has no non-matching bit; the
@@ -16,8 +17,6 @@
 
 namespace glide {
 namespace {
-
-constexpr int kThreads = 256;
 
 __device__ __forceinline__ uint32_t ordered_bits(float x) {
   uint32_t u = __float_as_uint(x);
@@ -48,36 +47,53 @@ __device__ __forceinline__ uint64_t wave_max_u64(uint64_t v) {
   return v;
 }
 
-__global__ __launch_bounds__(kThreads) void argmax_rows_kernel(const float* __restrict__ logits, int V,
-                                                               int32_t* __restrict__ idx) {
+// One 1024-thread workgroup per row; each thread requests 8 float4 (32
+// values) at once, so a 32000-entry row is a single round of loads.
+constexpr int kArgmaxThreads = 1024;
+constexpr int kArgmaxVec = 8;
+
+__global__ __launch_bounds__(kArgmaxThreads) void argmax_rows_kernel(const float* __restrict__ logits,
+                                                                     int V, int32_t* __restrict__ idx) {
   const int row = blockIdx.x, tid = threadIdx.x;
   const float* p = logits + (size_t)row * V;
   uint64_t best = 0;
   if ((V & 3) == 0 && (((uintptr_t)p) & 15) == 0) {
     const float4* p4 = (const float4*)p;
-    for (int i = tid; i < V / 4; i += kThreads) {
-      const float4 x = p4[i];
-      uint64_t k0 = argmax_key(x.x, 4 * i), k1 = argmax_key(x.y, 4 * i + 1);
-      uint64_t k2 = argmax_key(x.z, 4 * i + 2), k3 = argmax_key(x.w, 4 * i + 3);
-      k0 = k1 > k0 ? k1 : k0;
-      k2 = k3 > k2 ? k3 : k2;
-      k0 = k2 > k0 ? k2 : k0;
-      best = k0 > best ? k0 : best;
+    const int n4 = V / 4;
+    for (int i0 = 0; i0 < n4; i0 += kArgmaxThreads * kArgmaxVec) {
+      float4 x[kArgmaxVec];
+#pragma unroll
+      for (int u = 0; u < kArgmaxVec; ++u) {
+        const int i = i0 + tid + kArgmaxThreads * u;
+        x[u] = i < n4 ? p4[i] : make_float4(0.f, 0.f, 0.f, 0.f);
+      }
+#pragma unroll
+      for (int u = 0; u < kArgmaxVec; ++u) {
+        const int i = i0 + tid + kArgmaxThreads * u;
+        if (i < n4) {
+          uint64_t k0 = argmax_key(x[u].x, 4 * i), k1 = argmax_key(x[u].y, 4 * i + 1);
+          uint64_t k2 = argmax_key(x[u].z, 4 * i + 2), k3 = argmax_key(x[u].w, 4 * i + 3);
+          k0 = k1 > k0 ? k1 : k0;
+          k2 = k3 > k2 ? k3 : k2;
+          k0 = k2 > k0 ? k2 : k0;
+          best = k0 > best ? k0 : best;
+        }
+      }
     }
   } else {
-    for (int i = tid; i < V; i += kThreads) {
+    for (int i = tid; i < V; i += kArgmaxThreads) {
       const uint64_t k = argmax_key(p[i], i);
       best = k > best ? k : best;
     }
   }
   best = wave_max_u64(best);
-  __shared__ uint64_t per_wave[kThreads / 64];
+  __shared__ uint64_t per_wave[kArgmaxThreads / 64];
   if ((tid & 63) == 0) per_wave[tid >> 6] = best;
   __syncthreads();
-  if (tid == 0) {
-    uint64_t m = per_wave[0];
-    for (int w = 1; w < kThreads / 64; ++w) m = per_wave[w] > m ? per_wave[w] : m;
-    idx[row] = (int32_t)(0xFFFFFFFFu - (uint32_t)m);
+  if (tid < 64) {
+    uint64_t m = tid < kArgmaxThreads / 64 ? per_wave[tid] : 0;
+    m = wave_max_u64(m);
+    if (tid == 0) idx[row] = (int32_t)(0xFFFFFFFFu - (uint32_t)m);
   }
 }
 
@@ -128,7 +144,7 @@ __global__ __launch_bounds__(64) void tree_verify_kernel(const int32_t* __restri
 
 hipError_t launch_argmax_rows(const float* logits, int rows, int V, int32_t* idx,
                               hipStream_t stream) {
-  hipLaunchKernelGGL(argmax_rows_kernel, dim3(rows), dim3(kThreads), 0, stream, logits, V, idx);
+  hipLaunchKernelGGL(argmax_rows_kernel, dim3(rows), dim3(kArgmaxThreads), 0, stream, logits, V, idx);
   return hipGetLastError();
 }
 

@@ -97,9 +97,12 @@ def test_cape_rejects(lib, bad):
 
 
 def test_cape_workspace(lib):
-    assert lib.cape_expand_workspace(2, 5) == 2 * 5 * 8 * 8
-    assert lib.cape_expand_workspace(0, 5) == 0
-    assert lib.cape_expand_workspace(1, 65) == 0
+    # 32000 tokens = 8 parts of 4096, 8 keys of 8 bytes per part and row
+    assert lib.cape_expand_workspace(2, 5, 32000) == 2 * 5 * 8 * 8 * 8
+    assert lib.cape_expand_workspace(1, 1, 4096) == 8 * 8
+    assert lib.cape_expand_workspace(0, 5, 100) == 0
+    assert lib.cape_expand_workspace(1, 65, 100) == 0
+    assert lib.cape_expand_workspace(1, 5, 1) == 0
 
 
 @pytest.mark.parametrize("args", [
