@@ -407,13 +407,16 @@ template <class P, int NT, int QG, bool TREE>
 struct WaveTask {
   static constexpr int kWavesPerGroup = kWaves / QG;
   static constexpr int kStride = P::kStep * kWavesPerGroup;
-  // K/V steps in flight per wave: three for one query tile, two when the
-  // accumulators of two tiles need the registers.
-  static constexpr int kBufs = NT == 1 ? 3 : 2;
+  // K/V steps in flight per wave: two.  With one query tile this fits in
+  // 256 registers, so two waves share each SIMD (two workgroups per CU) and
+  // hide each other's dependency stalls; two tiles need the full register
+  // file (one wave per SIMD).
+  static constexpr int kBufs = 2;
 };
 
 template <class P, int NT, int QG, bool TREE>
-__global__ __launch_bounds__(kThreads) void tree_attn_kernel(AttnArgs args) {
+__global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(NT == 1 ? 2 : 1)))
+void tree_attn_kernel(AttnArgs args) {
   typedef typename P::elem_t elem_t;
   typedef WaveTask<P, NT, QG, TREE> Task;
   constexpr int kStep = P::kStep;
