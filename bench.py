@@ -176,17 +176,26 @@ def cpu_baseline(step, budget_s=12.0):
                          if wl.cross else "", total)}
 
 
+def kernel_source_hash():
+    import hashlib
+    src = b"".join(open(os.path.join(ROOT, "paper_2402_02082_amd", "csrc", n), "rb").read()
+                   for n in ("tree_attn.hip", "internal.h"))
+    return hashlib.sha256(src).hexdigest()[:16]
+
+
 def load_traffic():
-    """HBM bytes per tree-attention launch from the committed rocprofv3 PMC
-    summary, if one matches the current kernel build (else None)."""
+    """HBM bytes per verification attention call from the committed rocprofv3
+    counter summary, or None when the kernel source changed since then."""
     path = os.path.join(ROOT, "profiles", "tree_attn_vicuna7b_pmc.json")
     if not os.path.exists(path):
         return None
     try:
         rec = json.load(open(path))
-        return rec.get("traffic_bytes_per_launch")
     except (OSError, ValueError):
         return None
+    if rec.get("kernel_source_sha256_16") != kernel_source_hash():
+        return None
+    return rec.get("traffic_bytes_per_launch")
 
 
 def main():

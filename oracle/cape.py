@@ -12,7 +12,7 @@ Proposals"):
 4. expansion tokens are leaves: they are never used to predict later tokens;
 5. linearisation: the proposal first, then X_1, X_2, ... appended in order.
 
-Readings where the paper is silent (each listed in the design doc):
+Readings where the paper is silent:
 
 * ties in "highest probability" go to the lower token id (a strict total order
   (prob desc, id asc)); probabilities are compared as the float32 values given;

@@ -14,7 +14,7 @@ n + 1 is the target's greedy token after tree node n (it judges node n's
 children).  Both follow from the linearised tree: node n's logits row predicts
 the token after the path ending at n.
 
-Readings (the design doc lists them): the accept length is the depth of the deepest
+Readings where the paper is silent: the accept length is the depth of the deepest
 accepted node; when several accepted nodes share that depth the lowest node
 index wins; padding nodes (token -1) never match; no node accepted gives
 accept_len 0, last_node -1 and the bonus from slot 0.
