@@ -37,6 +37,8 @@
 #include <hip/hip_runtime.h>
 #include <stdint.h>
 
+#include <type_traits>
+
 #include "internal.h"
 
 namespace glide {
@@ -177,8 +179,16 @@ __device__ __forceinline__ __amdgpu_buffer_rsrc_t step_rsrc(const char* slab, in
                                            (short)0, rows * row_bytes, kBufferDesc3);
 }
 
+// Cache policy of the K/V loads: kStream marks them non-temporal (each row is
+// read once), which streams measurably faster when every K/V byte is
+// fetched by one wave; kKeep leaves the default policy for kernels whose
+// second query group re-reads each step from L2.
+constexpr int kKeep = 0;
+constexpr int kStream = 2;  // nt
+
+template <int CPOL>
 __device__ __forceinline__ u32x4_t load16(__amdgpu_buffer_rsrc_t r, int off) {
-  return __builtin_bit_cast(u32x4_t, __builtin_amdgcn_raw_buffer_load_b128(r, off, 0, 0));
+  return __builtin_bit_cast(u32x4_t, __builtin_amdgcn_raw_buffer_load_b128(r, off, 0, CPOL));
 }
 
 // Per-lane byte offsets inside one step, fixed for the whole loop.
@@ -194,19 +204,20 @@ __device__ __forceinline__ LaneOffsets lane_offsets(Bf16Path, int c, int g) {
                      (16 + 4 * g) * 256 + 16 * c};
 }
 
+template <int CPOL>
 __device__ __forceinline__ void load_kv(Bf16Path::KV& f, const char* kslab, const char* vslab,
                                         int j0, int k_end, const LaneOffsets& o) {
   const __amdgpu_buffer_rsrc_t rk = step_rsrc(kslab, j0, k_end, 256);
   const __amdgpu_buffer_rsrc_t rv = step_rsrc(vslab, j0, k_end, 256);
 #pragma unroll
   for (int st = 0; st < 4; ++st) {
-    f.k[0][st] = load16(rk, o.k0 + 64 * st);
-    f.k[1][st] = load16(rk, o.k1 + 64 * st);
+    f.k[0][st] = load16<CPOL>(rk, o.k0 + 64 * st);
+    f.k[1][st] = load16<CPOL>(rk, o.k1 + 64 * st);
   }
 #pragma unroll
   for (int i = 0; i < 4; ++i) {
-    f.v[i] = load16(rv, o.v0 + 256 * i);
-    f.v[4 + i] = load16(rv, o.v1 + 256 * i);
+    f.v[i] = load16<CPOL>(rv, o.v0 + 256 * i);
+    f.v[4 + i] = load16<CPOL>(rv, o.v1 + 256 * i);
   }
 }
 
@@ -216,17 +227,18 @@ __device__ __forceinline__ LaneOffsets lane_offsets(F32Path, int c, int g) {
   return LaneOffsets{c * 512 + 128 * g, 0, (4 * g) * 512 + 32 * c, 0};
 }
 
+template <int CPOL>
 __device__ __forceinline__ void load_kv(F32Path::KV& f, const char* kslab, const char* vslab, int j0,
                                         int k_end, const LaneOffsets& o) {
   const __amdgpu_buffer_rsrc_t rk = step_rsrc(kslab, j0, k_end, 512);
   const __amdgpu_buffer_rsrc_t rv = step_rsrc(vslab, j0, k_end, 512);
 #pragma unroll
-  for (int e = 0; e < 8; ++e) f.k[e] = __builtin_bit_cast(f32x4_t, load16(rk, o.k0 + 16 * e));
+  for (int e = 0; e < 8; ++e) f.k[e] = __builtin_bit_cast(f32x4_t, load16<CPOL>(rk, o.k0 + 16 * e));
 #pragma unroll
   for (int r = 0; r < 4; ++r)
 #pragma unroll
     for (int h = 0; h < 2; ++h)
-      f.v[r][h] = __builtin_bit_cast(f32x4_t, load16(rv, o.v0 + 512 * r + 16 * h));
+      f.v[r][h] = __builtin_bit_cast(f32x4_t, load16<CPOL>(rv, o.v0 + 512 * r + 16 * h));
 }
 
 // Online-softmax state of one 16-query tile for the lane's query column.
@@ -412,6 +424,7 @@ struct WaveTask {
   // hide each other's dependency stalls; two tiles need the full register
   // file (one wave per SIMD).
   static constexpr int kBufs = 2;
+  static constexpr int kCpol = QG == 1 ? kStream : kKeep;
 };
 
 template <class P, int NT, int QG, bool TREE>
@@ -455,7 +468,7 @@ void tree_attn_kernel(AttnArgs args) {
   const int full_end = min(Lcap, k_begin + args.chunk);
   typename P::KV buf[kBufs];
 #pragma unroll
-  for (int u = 0; u < kBufs; ++u) load_kv(buf[u], kslab, vslab, first + u * kStride, full_end, lo);
+  for (int u = 0; u < kBufs; ++u) load_kv<Task::kCpol>(buf[u], kslab, vslab, first + u * kStride, full_end, lo);
   __builtin_amdgcn_sched_barrier(0);
 
   const int Lb = min(max(raw_len, 0), TREE ? Lcap - N : Lcap);
@@ -468,7 +481,7 @@ void tree_attn_kernel(AttnArgs args) {
     // The split ends inside the cache: fetch again so that rows past the
     // sequence (possibly never written) read as zeros.
 #pragma unroll
-    for (int u = 0; u < kBufs; ++u) load_kv(buf[u], kslab, vslab, first + u * kStride, k_end, lo);
+    for (int u = 0; u < kBufs; ++u) load_kv<Task::kCpol>(buf[u], kslab, vslab, first + u * kStride, k_end, lo);
   }
 
   // Ancestor masks are only needed by the split that holds the tree rows.
@@ -502,7 +515,7 @@ void tree_attn_kernel(AttnArgs args) {
 #pragma unroll
     for (int u = 0; u < kBufs; ++u) {
       step<NT, TREE>(buf[u], qf, sm, acc, j, Lb, k_end, N, anc, args.scale_log2, g);
-      load_kv(buf[u], kslab, vslab, j + kBufs * kStride, k_end, lo);
+      load_kv<Task::kCpol>(buf[u], kslab, vslab, j + kBufs * kStride, k_end, lo);
       j += kStride;
     }
   }
@@ -572,6 +585,193 @@ void tree_attn_kernel(AttnArgs args) {
   }
 }
 
+// ---------------------------------------------------------------------------
+// Shared-step kernel for 17..64 query rows (bf16).  Each 32-key step is
+// fetched once per workgroup, straight from HBM into an LDS ring (buffer
+// loads with the `lds` modifier, against the same range-checked descriptors),
+// and consumed there by every wave that owns one of the sequence's 16-row
+// query tiles: with four tiles each wave owns one tile and walks every step;
+// with two tiles two waves share a tile and take alternate steps.  A round
+// is the set of steps the four waves consume together; the ring holds
+// kStages rounds, kStages - 1 of them in flight.
+//
+// LDS layout of one step: K rows then V rows, 32 rows x 256 B each, stored in
+// 16-byte units with unit (row, chunk) at row * 16 + (chunk ^ (row & 15)).
+// The loads write 64 consecutive units per instruction (four rows, chunks
+// permuted), so each instruction still reads 1 KB of contiguous HBM, and the
+// MFMA-operand reads (16 rows of one chunk, or 16 chunks of one row) hit 16
+// different bank groups.
+//
+// The compiler does not track LDS writes made by memory loads, so the ring
+// is synchronised by hand: each wave waits for its own loads of round r
+// (vmcnt) and a workgroup barrier publishes them and retires round r - 1,
+// whose stage is then refilled.
+// ---------------------------------------------------------------------------
+typedef __attribute__((address_space(3))) void* lds_ptr_t;
+
+constexpr int kStepBytes = 32 * 256 * 2;  // 32 keys of K and V (bf16)
+
+// Wait until at most N of this wave's vector-memory operations are in
+// flight, then meet the other waves -- without the release/acquire fences a
+// __syncthreads() carries (for memory-to-LDS loads those fences wait for
+// every outstanding load, which would drain the ring each round).  The
+// memory clobbers keep the compiler from moving LDS accesses across either.
+template <int N>
+__device__ __forceinline__ void ring_wait_and_meet() {
+  static_assert(N >= 0 && N < 64, "vmcnt range");
+  asm volatile("s_waitcnt vmcnt(%0)" ::"n"(N) : "memory");
+  asm volatile("s_barrier" ::: "memory");
+}
+
+__device__ __forceinline__ int swz_unit(int row, int chunk) { return row * 16 + (chunk ^ (row & 15)); }
+
+// K and V fragments of one step, read from its LDS copy (layouts as load_kv).
+__device__ __forceinline__ void read_step(Bf16Path::KV& f, const char* stepk, int c, int g) {
+  const char* stepv = stepk + kStepBytes / 2;
+#pragma unroll
+  for (int kt = 0; kt < 2; ++kt)
+#pragma unroll
+    for (int st = 0; st < 4; ++st)
+      f.k[kt][st] = *(const u32x4_t*)(stepk + 16 * swz_unit(16 * kt + c, 4 * st + g));
+#pragma unroll
+  for (int i = 0; i < 8; ++i)
+    f.v[i] = *(const u32x4_t*)(stepv + 16 * swz_unit(Bf16Path::key_slot(g, i), c));
+}
+
+template <int TQ, int LDS_BYTES, bool TREE>
+__global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(LDS_BYTES <= 65536 ? 2 : 1)))
+void tree_attn_shared_kernel(AttnArgs args) {
+  constexpr int kWpt = kWaves / TQ;                // waves per query tile
+  constexpr int kRoundBytes = kWpt * kStepBytes;   // steps consumed together
+  constexpr int kStages = LDS_BYTES / kRoundBytes;
+  constexpr int kInstr = kRoundBytes / 1024 / kWaves;  // 1 KB loads per wave per round
+  constexpr int kRoundKeys = 32 * kWpt;
+  static_assert(kStages >= 2, "ring needs two stages");
+  __shared__ __attribute__((aligned(1024))) char ring[LDS_BYTES];
+
+  const int s = blockIdx.x, h = blockIdx.y, b = blockIdx.z;
+  const int tid = threadIdx.x, lane = tid & 63;
+  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+  const int c = lane & 15, g = lane >> 4;
+  const int tile = wave % TQ, phase = wave / TQ;
+  const int N = args.N, H = args.H, Lcap = args.L_cap;
+
+  const int Lb = min(max(args.seq_lens[b], 0), TREE ? Lcap - N : Lcap);
+  const int T = Lb + (TREE ? N : 0);
+  const int nsplit = max(1, (T + args.chunk - 1) / args.chunk);
+  if (s >= nsplit) return;
+  const int k_begin = s * args.chunk;
+  const int k_end = min(T, k_begin + args.chunk);
+  const int rounds = k_end > k_begin ? (k_end - k_begin + kRoundKeys - 1) / kRoundKeys : 0;
+
+  const size_t head_off = ((size_t)b * H + h) * (size_t)Lcap * kD;
+  const char* kslab = (const char*)((const uint16_t*)args.k + head_off);
+  const char* vslab = (const char*)((const uint16_t*)args.v + head_off);
+
+  int my_parent = -1;
+  if (TREE && lane < N) my_parent = args.parents[(size_t)b * N + lane];
+  const int n = 16 * tile + c;
+  const bool tile_live = 16 * tile < N;
+  Bf16Path::QFrag qf[1];
+  load_q<Bf16Path>(qf[0], (const uint16_t*)args.q + (((size_t)b * N + min(n, N - 1)) * H + h) * kD,
+                   n < N, g);
+
+  // This wave's share of a round: instruction k moves 1 KB (rows 4i..4i+3 of
+  // one matrix of one step, i = wave + 4 * (k & 1)); lanes fetch their unit's
+  // chunk so the swizzled layout lands in place.
+  const int dma_row = 4 * wave + (lane >> 4);
+  const int dma_off = dma_row * 256 + 16 * ((lane & 15) ^ (dma_row & 15));
+  auto issue_round = [&](int r) {
+    char* stage = ring + (r % kStages) * kRoundBytes;
+#pragma unroll
+    for (int k = 0; k < kInstr; ++k) {
+      const int p = k / 4, m = (k / 2) & 1, hi = k & 1;
+      const int j0 = k_begin + r * kRoundKeys + 32 * p;
+      const __amdgpu_buffer_rsrc_t rs = step_rsrc(m ? vslab : kslab, j0, k_end, 256);
+      char* dst = stage + p * kStepBytes + m * (kStepBytes / 2) + (wave + 4 * hi) * 1024;
+      __builtin_amdgcn_raw_ptr_buffer_load_lds(rs, (lds_ptr_t)dst, 16, dma_off + 4096 * hi, 0, 0,
+                                               kStream);
+    }
+  };
+#pragma unroll
+  for (int r = 0; r < kStages - 1; ++r) issue_round(r);
+
+  uint64_t anc[1] = {0};
+  if (TREE && k_end > Lb) anc[0] = shfl_u64(ancestor_mask_from(my_parent, N, lane), min(n, 63));
+
+  SoftmaxState sm[1];
+  sm[0].m = neg_inf();
+  sm[0].l = 0.f;
+  f32x4_t acc[1][8];
+#pragma unroll
+  for (int t = 0; t < 8; ++t) acc[0][t] = f32x4_t{0.f, 0.f, 0.f, 0.f};
+
+  for (int r = 0; r < rounds; ++r) {
+    // this wave's loads of round r have landed; after the barrier everyone's
+    // have, and round r - 1 is retired
+    ring_wait_and_meet<(kStages - 2) * kInstr>();
+    issue_round(r + kStages - 1);
+    const int j0 = k_begin + r * kRoundKeys + 32 * phase;
+    if (tile_live && j0 < k_end) {
+      Bf16Path::KV f;
+      read_step(f, ring + (r % kStages) * kRoundBytes + phase * kStepBytes, c, g);
+      if (j0 + 32 > k_end) {
+        // rows past the split were not written by this round's loads
+#pragma unroll
+        for (int i = 0; i < 8; ++i)
+          if (j0 + Bf16Path::key_slot(g, i) >= k_end) f.v[i] = u32x4_t{0, 0, 0, 0};
+      }
+      step<1, TREE>(f, qf, sm, acc, j0, Lb, k_end, N, anc, args.scale_log2, g);
+    }
+  }
+  asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
+  __syncthreads();  // the ring is free for the merge below
+  sm[0].l = sum_across_groups(sm[0].l);
+
+  // Waves sharing a tile merge through LDS; phase 0 finishes the tile.
+  float* mo = (float*)ring;                      // [TQ][8][4][64]
+  float* mm = mo + TQ * 8 * 4 * 64;              // [TQ][64]
+  float* ml = mm + TQ * 64;
+  if (kWpt > 1 && phase == 1) {
+    mm[tile * 64 + lane] = sm[0].m;
+    ml[tile * 64 + lane] = sm[0].l;
+#pragma unroll
+    for (int t = 0; t < 8; ++t)
+#pragma unroll
+      for (int r = 0; r < 4; ++r) mo[((tile * 8 + t) * 4 + r) * 64 + lane] = acc[0][t][r];
+  }
+  if (kWpt > 1) __syncthreads();
+  if (phase != 0 || !tile_live) return;
+  float M = sm[0].m, f0 = 1.f, f1 = 0.f, L = sm[0].l;
+  if (kWpt > 1) {
+    const float m1 = mm[tile * 64 + lane];
+    M = fmaxf(sm[0].m, m1);
+    f0 = (M == neg_inf()) ? 0.f : fast_exp2(sm[0].m - M);
+    f1 = (M == neg_inf()) ? 0.f : fast_exp2(m1 - M);
+    L = f0 * sm[0].l + f1 * ml[tile * 64 + lane];
+  }
+  const float inv = (nsplit == 1) ? ((L > 0.f) ? 1.f / L : 0.f) : 1.f;
+  const size_t part_base = (((size_t)b * H + h) * args.splits + s) * N;
+#pragma unroll
+  for (int r = 0; r < 4; ++r) {
+    float o[8];
+#pragma unroll
+    for (int t = 0; t < 8; ++t) {
+      float v = f0 * acc[0][t][r];
+      if (kWpt > 1) v += f1 * mo[((tile * 8 + t) * 4 + r) * 64 + lane];
+      o[t] = v * inv;
+    }
+    if (n < N) {
+      const int d = 32 * g + 8 * r;
+      if (nsplit == 1)
+        store_row8((uint16_t*)args.out + (((size_t)b * N + n) * H + h) * kD + d, o);
+      else
+        store_row8(args.part_o + (part_base + n) * kD + d, o);
+    }
+  }
+  if (nsplit > 1 && n < N && g == 0) args.part_ml[part_base + n] = make_float2(M, L);
+}
+
 // Merges the split partial states of every (sequence, head) whose keys were
 // divided, in a fixed split order (the result does not depend on timing).
 // One wave per output row (sequence, query, head); each lane owns two head
@@ -631,12 +831,21 @@ __global__ __launch_bounds__(kThreads) void tree_attn_combine(AttnArgs args) {
   store_2((elem_t*)args.out + (size_t)row * kD + 2 * lane, o0 * inv, o1 * inv);
 }
 
+// LDS ring sizes of the shared-step kernel: 64 KB (two workgroups per CU)
+// for four tiles, 128 KB for two tiles (rounds of two steps).
+constexpr int kSharedLds4 = 65536;
+constexpr int kSharedLds2 = 131072;
+
 template <class P, bool TREE>
 hipError_t launch_nt(const AttnArgs& a, hipStream_t stream) {
   const dim3 grid(a.splits, a.H, a.B), block(kThreads);
   const int tiles = (a.N + 15) / 16;
   if (tiles == 1)
     hipLaunchKernelGGL((tree_attn_kernel<P, 1, 1, TREE>), grid, block, 0, stream, a);
+  else if (std::is_same<P, Bf16Path>::value && tiles == 2)
+    hipLaunchKernelGGL((tree_attn_shared_kernel<2, kSharedLds2, TREE>), grid, block, 0, stream, a);
+  else if (std::is_same<P, Bf16Path>::value)
+    hipLaunchKernelGGL((tree_attn_shared_kernel<4, kSharedLds4, TREE>), grid, block, 0, stream, a);
   else if (tiles == 2)
     hipLaunchKernelGGL((tree_attn_kernel<P, 2, 1, TREE>), grid, block, 0, stream, a);
   else
