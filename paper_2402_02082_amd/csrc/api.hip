@@ -49,7 +49,7 @@ bool parents_ok(const std::vector<int32_t>& parents, int B, int N) {
 }
 
 bool tree_attn_sizes_ok(int B, int N, int H, int D, int L_cap, bool tree) {
-  if (B < 1 || H < 1 || N < 1 || N > glide::kMaxNodes) return false;
+  if (B < 1 || B > 65535 || H < 1 || N < 1 || N > glide::kMaxNodes) return false;  // B is a grid dim
   if (D != glide::kHeadDim) return false;
   if (L_cap < (tree ? N : 1)) return false;
   // keep every element offset inside size_t and every key index inside int

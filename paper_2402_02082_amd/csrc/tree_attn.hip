@@ -437,7 +437,7 @@ void tree_attn_kernel(AttnArgs args) {
   constexpr int kWpg = Task::kWavesPerGroup;
   constexpr int kStride = Task::kStride;
 
-  const int s = blockIdx.x, h = blockIdx.y, b = blockIdx.z;
+  const int h = blockIdx.x, b = blockIdx.y, s = blockIdx.z;
   const int tid = threadIdx.x, lane = tid & 63;
   const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
   const int c = lane & 15, g = lane >> 4;
@@ -649,7 +649,7 @@ void tree_attn_shared_kernel(AttnArgs args) {
   static_assert(kStages >= 2, "ring needs two stages");
   __shared__ __attribute__((aligned(1024))) char ring[LDS_BYTES];
 
-  const int s = blockIdx.x, h = blockIdx.y, b = blockIdx.z;
+  const int h = blockIdx.x, b = blockIdx.y, s = blockIdx.z;
   const int tid = threadIdx.x, lane = tid & 63;
   const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
   const int c = lane & 15, g = lane >> 4;
@@ -831,14 +831,18 @@ __global__ __launch_bounds__(kThreads) void tree_attn_combine(AttnArgs args) {
   store_2((elem_t*)args.out + (size_t)row * kD + 2 * lane, o0 * inv, o1 * inv);
 }
 
-// LDS ring sizes of the shared-step kernel: 64 KB (two workgroups per CU)
-// for four tiles, 128 KB for two tiles (rounds of two steps).
+// LDS ring of the shared-step kernel: 64 KB, so two workgroups share a CU
+// (four stages of one step for four tiles, two stages of two steps for two
+// tiles).  Larger rings hold one workgroup per CU and measured slower.
 constexpr int kSharedLds4 = 65536;
-constexpr int kSharedLds2 = 131072;
+constexpr int kSharedLds2 = 65536;
 
 template <class P, bool TREE>
 hipError_t launch_nt(const AttnArgs& a, hipStream_t stream) {
-  const dim3 grid(a.splits, a.H, a.B), block(kThreads);
+  // Heads vary fastest and splits slowest: workgroups are handed to the XCDs
+  // round-robin by linear id, so every split level spreads over all eight
+  // XCDs, and the empty splits of short sequences sit at the end of the grid.
+  const dim3 grid(a.H, a.B, a.splits), block(kThreads);
   const int tiles = (a.N + 15) / 16;
   if (tiles == 1)
     hipLaunchKernelGGL((tree_attn_kernel<P, 1, 1, TREE>), grid, block, 0, stream, a);
@@ -860,6 +864,16 @@ hipError_t launch_nt(const AttnArgs& a, hipStream_t stream) {
 
 }  // namespace
 
+// Relative cost of s splits: the grid runs in ceil(B*H*s / CUs) waves of
+// workgroups, each 1/s of a sequence long, and every split adds its partial
+// results (written once, read once by the merge) to the K/V stream.
+static double split_cost(long bh, int s, int N, int L_cap) {
+  const double kv = (double)L_cap * kHeadDim * 2 * 2;                // K and V, bf16
+  const double part = (double)N * (kHeadDim + 2) * sizeof(float);  // one split's partials
+  const double waves = (double)((bh * s + kNumCU - 1) / kNumCU);
+  return waves / s * (1.0 + (s > 1 ? 2.0 * s * part / kv : 0.0));
+}
+
 AttnPlan plan_tree_attn(int B, int N, int H, int L_cap, int max_splits) {
   AttnPlan p{};
   const int keys = L_cap;  // upper bound on the keys any query sees
@@ -868,10 +882,18 @@ AttnPlan plan_tree_attn(int B, int N, int H, int L_cap, int max_splits) {
   if (max_splits > 0) {
     want = max_splits;
   } else {
-    // One 4-wave workgroup fills a CU; split until the grid covers the CUs
-    // once, keeping at least kMinChunk keys per split.
-    want = (int)(kNumCU / bh);
-    want = min(want, (keys + kMinChunk - 1) / kMinChunk);
+    // Split only where it balances the CUs clearly better (a fifth less
+    // cost), taking the fewest splits that reach the best cost, and keep
+    // at least kMinChunk keys per split.
+    const int most = min(kMaxSplits, (keys + kMinChunk - 1) / kMinChunk);
+    const double one = split_cost(bh, 1, N, L_cap);
+    double best = one;
+    want = 1;
+    for (int s = 2; s <= most; ++s) {
+      const double c = split_cost(bh, s, N, L_cap);
+      if (c < best - 1e-9) best = c, want = s;
+    }
+    if (best > 0.8 * one) want = 1;
   }
   want = max(1, min(want, kMaxSplits));
   int chunk = (keys + want - 1) / want;
