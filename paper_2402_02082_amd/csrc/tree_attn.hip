@@ -508,14 +508,23 @@ void tree_attn_kernel(AttnArgs args) {
   // the step kBufs ahead.  The trip count is rounded up to whole rounds of
   // kBufs steps so the body is straight-line code and every wait leaves the
   // other buffers' loads in flight; steps at or past k_end read zeros and
-  // are fully masked.
+  // are fully masked (the last round skips them).
   const int iters = (nsteps + kBufs - 1) / kBufs;
   int j = first;
-  for (int it = 0; it < iters; ++it) {
+  for (int it = 0; it + 1 < iters; ++it) {
 #pragma unroll
     for (int u = 0; u < kBufs; ++u) {
       step<NT, TREE>(buf[u], qf, sm, acc, j, Lb, k_end, N, anc, args.scale_log2, g);
       load_kv<Task::kCpol>(buf[u], kslab, vslab, j + kBufs * kStride, k_end, lo);
+      j += kStride;
+    }
+  }
+  // Last round without refills: a load issued past the final step would
+  // only hold up the merge below, which must wait for its registers.
+  if (iters > 0) {
+#pragma unroll
+    for (int u = 0; u < kBufs; ++u) {
+      if (u == 0 || j < k_end) step<NT, TREE>(buf[u], qf, sm, acc, j, Lb, k_end, N, anc, args.scale_log2, g);
       j += kStride;
     }
   }
@@ -592,8 +601,9 @@ void tree_attn_kernel(AttnArgs args) {
 // and consumed there by every wave that owns one of the sequence's 16-row
 // query tiles: with four tiles each wave owns one tile and walks every step;
 // with two tiles two waves share a tile and take alternate steps.  A round
-// is the set of steps the four waves consume together; the ring holds
-// kStages rounds, kStages - 1 of them in flight.
+// is the set of steps the four waves consume together (one or two).  The
+// ring holds kStages steps: while a round is read, the rest are in flight,
+// and the loads of a round go out as soon as the round before it retires.
 //
 // LDS layout of one step: K rows then V rows, 32 rows x 256 B each, stored in
 // 16-byte units with unit (row, chunk) at row * 16 + (chunk ^ (row & 15)).
@@ -639,14 +649,13 @@ __device__ __forceinline__ void read_step(Bf16Path::KV& f, const char* stepk, in
 }
 
 template <int TQ, int LDS_BYTES, bool TREE>
-__global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(LDS_BYTES <= 65536 ? 2 : 1)))
+__global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(2 * LDS_BYTES <= 163840 ? 2 : 1)))
 void tree_attn_shared_kernel(AttnArgs args) {
   constexpr int kWpt = kWaves / TQ;                // waves per query tile
-  constexpr int kRoundBytes = kWpt * kStepBytes;   // steps consumed together
-  constexpr int kStages = LDS_BYTES / kRoundBytes;
-  constexpr int kInstr = kRoundBytes / 1024 / kWaves;  // 1 KB loads per wave per round
-  constexpr int kRoundKeys = 32 * kWpt;
-  static_assert(kStages >= 2, "ring needs two stages");
+  constexpr int kStages = LDS_BYTES / kStepBytes;        // ring stages, one step each
+  constexpr int kStepInstr = kStepBytes / 1024 / kWaves;  // 1 KB loads per wave per step
+  constexpr int kRoundKeys = 32 * kWpt;                   // a round: kWpt steps
+  static_assert(kStages >= 2 * kWpt && kStages * kStepBytes == LDS_BYTES, "ring of two rounds or more");
   __shared__ __attribute__((aligned(1024))) char ring[LDS_BYTES];
 
   const int h = blockIdx.x, b = blockIdx.y, s = blockIdx.z;
@@ -676,25 +685,27 @@ void tree_attn_shared_kernel(AttnArgs args) {
   load_q<Bf16Path>(qf[0], (const uint16_t*)args.q + (((size_t)b * N + min(n, N - 1)) * H + h) * kD,
                    n < N, g);
 
-  // This wave's share of a round: instruction k moves 1 KB (rows 4i..4i+3 of
-  // one matrix of one step, i = wave + 4 * (k & 1)); lanes fetch their unit's
-  // chunk so the swizzled layout lands in place.
+  // This wave's share of step t: instruction k moves 1 KB (rows 4i..4i+3 of
+  // K or V, i = wave + 4 * (k & 1)) into stage t % kStages; lanes fetch their
+  // unit's chunk so the swizzled layout lands in place.
   const int dma_row = 4 * wave + (lane >> 4);
   const int dma_off = dma_row * 256 + 16 * ((lane & 15) ^ (dma_row & 15));
-  auto issue_round = [&](int r) {
-    char* stage = ring + (r % kStages) * kRoundBytes;
+  auto issue_step = [&](int t) {
+    char* stage = ring + (t % kStages) * kStepBytes;
+    const int j0 = k_begin + 32 * t;
 #pragma unroll
-    for (int k = 0; k < kInstr; ++k) {
-      const int p = k / 4, m = (k / 2) & 1, hi = k & 1;
-      const int j0 = k_begin + r * kRoundKeys + 32 * p;
+    for (int k = 0; k < kStepInstr; ++k) {
+      const int m = k / 2, hi = k & 1;
       const __amdgpu_buffer_rsrc_t rs = step_rsrc(m ? vslab : kslab, j0, k_end, 256);
-      char* dst = stage + p * kStepBytes + m * (kStepBytes / 2) + (wave + 4 * hi) * 1024;
+      char* dst = stage + m * (kStepBytes / 2) + (wave + 4 * hi) * 1024;
       __builtin_amdgcn_raw_ptr_buffer_load_lds(rs, (lds_ptr_t)dst, 16, dma_off + 4096 * hi, 0, 0,
                                                kStream);
     }
   };
+  // Round r issues steps kStages - kWpt + kWpt * r + i (i < kWpt), into the
+  // stages of round r - 1; the prologue issues the steps before those.
 #pragma unroll
-  for (int r = 0; r < kStages - 1; ++r) issue_round(r);
+  for (int t = 0; t < kStages - kWpt; ++t) issue_step(t);
 
   uint64_t anc[1] = {0};
   if (TREE && k_end > Lb) anc[0] = shfl_u64(ancestor_mask_from(my_parent, N, lane), min(n, 63));
@@ -707,14 +718,17 @@ void tree_attn_shared_kernel(AttnArgs args) {
   for (int t = 0; t < 8; ++t) acc[0][t] = f32x4_t{0.f, 0.f, 0.f, 0.f};
 
   for (int r = 0; r < rounds; ++r) {
-    // this wave's loads of round r have landed; after the barrier everyone's
-    // have, and round r - 1 is retired
-    ring_wait_and_meet<(kStages - 2) * kInstr>();
-    issue_round(r + kStages - 1);
-    const int j0 = k_begin + r * kRoundKeys + 32 * phase;
+    // this wave's loads of round r have landed (at most the steps issued
+    // after it, kStages - 2 * kWpt of them, are pending); after the barrier
+    // everyone's have, and round r - 1 is retired
+    ring_wait_and_meet<(kStages - 2 * kWpt) * kStepInstr>();
+#pragma unroll
+    for (int i = 0; i < kWpt; ++i) issue_step(kStages - kWpt + kWpt * r + i);
+    const int t = kWpt * r + phase;
+    const int j0 = k_begin + 32 * t;
     if (tile_live && j0 < k_end) {
       Bf16Path::KV f;
-      read_step(f, ring + (r % kStages) * kRoundBytes + phase * kStepBytes, c, g);
+      read_step(f, ring + (t % kStages) * kStepBytes, c, g);
       if (j0 + 32 > k_end) {
         // rows past the split were not written by this round's loads
 #pragma unroll
@@ -831,9 +845,9 @@ __global__ __launch_bounds__(kThreads) void tree_attn_combine(AttnArgs args) {
   store_2((elem_t*)args.out + (size_t)row * kD + 2 * lane, o0 * inv, o1 * inv);
 }
 
-// LDS ring of the shared-step kernel: 64 KB, so two workgroups share a CU
-// (four stages of one step for four tiles, two stages of two steps for two
-// tiles).  Larger rings hold one workgroup per CU and measured slower.
+// LDS rings of the shared-step kernel: four 16 KB steps, so two workgroups
+// share a CU.  Rings past 80 KB hold one workgroup per CU and measured
+// slower; a five-step ring helps only grids of at most one workgroup per CU.
 constexpr int kSharedLds4 = 65536;
 constexpr int kSharedLds2 = 65536;
 
