@@ -21,8 +21,10 @@ Prints one JSON line.  `value` is the attention bytes per step (K/V rows read,
 Q read, O written in every attention call of the step; the algorithmic count,
 split partials excluded) divided by the GPU time of the whole step, replayed
 as a HIP graph so that host launch overhead is not timed.  `roofline` is the
-verification attention call (attention kernel + split merge) timed with HIP
-events around each call.
+verification attention call (attention kernel + split merge): HIP events
+around graph replays of the verification step, divided by its call count.
+`other_configs` repeats the measurement for every other workload, and
+`stream_probe` gives the streaming rates of plain torch kernels for context.
 """
 
 import argparse
@@ -194,6 +196,104 @@ def load_traffic():
     return rec.get("traffic_bytes_per_launch")
 
 
+def measure(wl, steps, warmup, max_splits):
+    """Builds a workload's step, captures it (and its verification layers
+    alone) as HIP graphs, and times both with HIP events around the replays."""
+    step = Step(wl, torch.bfloat16, SEED, max_splits)
+    torch.cuda.synchronize()
+    # Capture one whole step, and the verification layers alone, as HIP
+    # graphs (the library never allocates, so both replay as captured).
+    side = torch.cuda.Stream()
+    side.wait_stream(torch.cuda.current_stream())
+    with torch.cuda.stream(side):
+        for _ in range(max(warmup, 1)):
+            step.run()
+    torch.cuda.current_stream().wait_stream(side)
+    torch.cuda.synchronize()
+    g_step, g_verify = torch.cuda.CUDAGraph(), torch.cuda.CUDAGraph()
+    with torch.cuda.graph(g_step):
+        step.run()
+    with torch.cuda.graph(g_verify):
+        step.run_verify_layers()
+    torch.cuda.synchronize()
+    for _ in range(warmup):
+        g_step.replay()
+    torch.cuda.synchronize()
+
+    # Timed region 1: K whole steps (graph replays).
+    start, stop = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    start.record()
+    for _ in range(steps):
+        g_step.replay()
+    stop.record()
+    torch.cuda.synchronize()
+    ms_step = start.elapsed_time(stop) / steps
+    planted_ok = bool(np.array_equal(step.acc.cpu().numpy(), step.planted))
+
+    # Timed region 2: the verification step alone (the L attention calls).
+    start.record()
+    for _ in range(steps):
+        g_verify.replay()
+    stop.record()
+    torch.cuda.synchronize()
+    verify_us = start.elapsed_time(stop) / steps * 1e3
+    del g_step, g_verify
+    return step, {"ms_step": ms_step, "verify_us": verify_us, "planted_ok": planted_ok}
+
+
+def other_configs(skip, steps, warmup, max_splits):
+    """The verification step and the whole step of every other workload,
+    measured as the headline one (same seed, graphs, events)."""
+    out = []
+    for i in sorted(W.WORKLOADS):
+        if i == skip:
+            continue
+        wl = W.WORKLOADS[i]
+        step, t = measure(wl, steps, warmup, max_splits)
+        vgbps = step.verify_bytes * wl.layers / (t["verify_us"] * 1e-6) / 1e9
+        sbytes = step.verify_bytes * wl.layers + step.cross_bytes
+        out.append({"workload": wl.name, "layers": wl.layers, "batch": wl.batch,
+                    "tree_nodes": wl.nodes,
+                    "us_per_verify_step": round(t["verify_us"], 2),
+                    "us_per_verify_call": round(t["verify_us"] / wl.layers, 2),
+                    "verify_step_gbps": round(vgbps, 1),
+                    "verify_frac_of_hbm_peak": round(vgbps / HBM_PEAK_GBPS, 4),
+                    "ms_per_step": round(t["ms_step"], 4),
+                    "step_gbps": round(sbytes / (t["ms_step"] * 1e-3) / 1e9, 1),
+                    "planted_accept_len_ok": t["planted_ok"]})
+        del step
+        torch.cuda.empty_cache()
+    return out
+
+
+def stream_probe():
+    """Measured streaming rates of plain torch kernels, for context: a
+    reduction that reads 4 GiB, and a 2 GiB device-to-device copy."""
+    x = torch.zeros(2 << 30, dtype=torch.bfloat16, device="cuda")
+    y = torch.empty(1 << 30, dtype=torch.bfloat16, device="cuda")
+    start, stop = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    x.sum()
+    torch.cuda.synchronize()
+    start.record()
+    for _ in range(10):
+        x.sum()
+    stop.record()
+    torch.cuda.synchronize()
+    read = x.numel() * 2 * 10 / (start.elapsed_time(stop) * 1e-3) / 1e9
+    src = x[: y.numel()]
+    y.copy_(src)
+    start.record()
+    for _ in range(10):
+        y.copy_(src)
+    stop.record()
+    torch.cuda.synchronize()
+    copy = 2 * y.numel() * 2 * 10 / (start.elapsed_time(stop) * 1e-3) / 1e9
+    del x, y
+    torch.cuda.empty_cache()
+    return {"read_gbps": round(read, 1), "copy_gbps": round(copy, 1),
+            "kernels": "torch sum over 4 GiB bf16 (read), torch copy of 2 GiB (read + write)"}
+
+
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -202,6 +302,8 @@ def main():
     ap.add_argument("--workload", type=int, default=2, choices=sorted(W.WORKLOADS))
     ap.add_argument("--max-splits", type=int, default=0)
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--headline-only", action="store_true",
+                    help="skip the other workloads and the streaming probe")
     ap.add_argument("--calibrate-copy-mib", type=int, default=0,
                     help="only run a plain device-to-device copy of this many MiB (five times), "
                          "for scaling HBM traffic counters; prints nothing else")
@@ -225,47 +327,8 @@ def main():
     glide.load()
 
     wl = W.WORKLOADS[args.workload]
-    dtype = torch.bfloat16
-    step = Step(wl, dtype, SEED, args.max_splits)
-    torch.cuda.synchronize()
-
-    # Capture one whole step, and the verification layers alone, as HIP
-    # graphs (the library never allocates, so both replay as captured).
-    side = torch.cuda.Stream()
-    side.wait_stream(torch.cuda.current_stream())
-    with torch.cuda.stream(side):
-        for _ in range(max(args.warmup, 1)):
-            step.run()
-    torch.cuda.current_stream().wait_stream(side)
-    torch.cuda.synchronize()
-    g_step, g_verify = torch.cuda.CUDAGraph(), torch.cuda.CUDAGraph()
-    with torch.cuda.graph(g_step):
-        step.run()
-    with torch.cuda.graph(g_verify):
-        step.run_verify_layers()
-    torch.cuda.synchronize()
-    for _ in range(args.warmup):
-        g_step.replay()
-    torch.cuda.synchronize()
-
-    # Timed region 1: K whole steps (graph replays).
-    start, stop = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
-    start.record()
-    for _ in range(args.steps):
-        g_step.replay()
-    stop.record()
-    torch.cuda.synchronize()
-    ms_step = start.elapsed_time(stop) / args.steps
-    acc = step.acc.cpu().numpy()
-    planted_ok = bool(np.array_equal(acc, step.planted))
-
-    # Timed region 2: the verification step alone (the L attention calls).
-    start.record()
-    for _ in range(args.steps):
-        g_verify.replay()
-    stop.record()
-    torch.cuda.synchronize()
-    verify_us = start.elapsed_time(stop) / args.steps * 1e3
+    step, t = measure(wl, args.steps, args.warmup, args.max_splits)
+    ms_step, verify_us, planted_ok = t["ms_step"], t["verify_us"], t["planted_ok"]
 
     # The dominant kernel's launch: one glide_tree_attn call (attention kernel
     # + split merge) of the verification pass, averaged over the calls of
@@ -309,6 +372,12 @@ def main():
     }
     if not args.no_cpu_baseline:
         rec["cpu_baseline"] = cpu_baseline(step)
+    if not args.headline_only:
+        del step
+        torch.cuda.empty_cache()
+        rec["other_configs"] = other_configs(args.workload, max(3, min(args.steps, 10)),
+                                             max(1, min(args.warmup, 2)), args.max_splits)
+        rec["stream_probe"] = stream_probe()
     print(json.dumps(rec), flush=True)
 
 
