@@ -91,13 +91,13 @@ class Step:
         self.bonus = torch.empty((B,), dtype=torch.int32, device=dev)
         L_cap = wl.l_cap
         self.ws = glide.attn_workspace(B, N, wl.heads, L_cap, max_splits, dev)
-        self.xws = (glide.attn_workspace(B, wl.depth, wl.heads, L_cap, max_splits, dev)
+        self.xws = (glide.attn_workspace(B, wl.cross_queries, wl.heads, L_cap, max_splits, dev)
                     if wl.cross else None)
         self.cape_ws = torch.empty(max(glide.load().cape_expand_workspace(B, wl.depth, V), 1),
                                    dtype=torch.uint8, device=dev)
         elem = 2 if dtype == torch.bfloat16 else 4
         self.verify_bytes = attn_bytes(self.lens_np, N, wl.heads, elem, True)
-        self.cross_bytes = attn_bytes(self.lens_np, wl.depth, wl.heads, elem, False) \
+        self.cross_bytes = attn_bytes(self.lens_np, wl.cross_queries, wl.heads, elem, False) \
             if wl.cross else 0
 
     def tree(self):
@@ -355,7 +355,7 @@ def main():
                    "head_dim": wl.head_dim, "batch": wl.batch,
                    "prefix": [int(x) for x in step.lens_np], "tree_nodes": wl.nodes,
                    "tree_depth": wl.depth, "top_k": wl.k, "vocab": wl.vocab,
-                   "cross_attn_queries": wl.depth if wl.cross else 0, "seed": SEED},
+                   "cross_attn_queries": wl.cross_queries, "seed": SEED},
         "us_per_verify_step": round(verify_us, 2),
         "verify_step_gbps": round(step.verify_bytes * wl.layers / (verify_us * 1e-6) / 1e9, 2),
         "hbm_frac_of_step": round(value / HBM_PEAK_GBPS, 4),

@@ -53,7 +53,8 @@ class Workload:
     k: int              # expansion cap used to build the attention tree
     k_config: int       # the workload's stated top-k (separate CaPE parity runs)
     tree: str           # "chain" or "cape"
-    cross: bool         # also one GliDe cross-attention layer (gamma queries)
+    cross: bool         # also one GliDe cross-attention layer
+    cross_queries: int = 0  # its query rows per sequence (0 when there is none)
     vocab: int = VOCAB
     head_dim: int = HEAD_DIM
 
@@ -67,7 +68,7 @@ WORKLOADS = {
     1: Workload("7b-1layer-chain5", 1, 32, 1, 512, 512, 5, 5, 0, 0, "chain", False),
     # Vicuna-7B: 32 layers, prefix 2048, 16-node CaPE tree of depth 5, k = 3,
     # plus one 5-query GliDe cross-attention layer on the same cache.
-    2: Workload("vicuna7b-cape16", 32, 32, 1, 2048, 2048, 16, 5, 3, 3, "cape", True),
+    2: Workload("vicuna7b-cape16", 32, 32, 1, 2048, 2048, 16, 5, 3, 3, "cape", True, 5),
     # Vicuna-13B: 40 layers x 40 heads, B = 4, prefixes U[1024, 4096], 32 nodes,
     # depth 6.  k = 4 gives only 6 + 24 = 30 nodes, so the attention tree uses
     # the uncapped S(p) (k = 7) to reach 32; k = 4 runs as its own CaPE case.
@@ -76,8 +77,9 @@ WORKLOADS = {
     # depth 8 (k = 5 gives 48 nodes; the attention tree uses k = 7).
     4: Workload("vicuna33b-cape64", 60, 52, 8, 4096, 8192, 64, 8, 7, 5, "cape", False),
     # Long context at 7B head shape: 4 layers, B = 16, prefixes U[16384, 32768],
-    # 64-node trees of depth 8, plus a cross-attention layer per sequence.
-    5: Workload("7b-longctx-cape64", 4, 32, 16, 16384, 32768, 64, 8, 7, 7, "cape", True),
+    # 64-node trees of depth 8, plus a 5-query cross-attention layer per
+    # sequence (the stated query count, not the tree depth).
+    5: Workload("7b-longctx-cape64", 4, 32, 16, 16384, 32768, 64, 8, 7, 7, "cape", True, 5),
 }
 
 
@@ -240,8 +242,8 @@ def attention_layer(wl, seed, layer, dtype, device, batch=None, heads=None, l_ca
 
 
 def cross_queries(wl, seed, dtype, device):
-    """GliDe cross-attention queries [B, gamma, H, D] (one draft layer)."""
+    """GliDe cross-attention queries [B, Nq, H, D] (one draft layer)."""
     import torch
     g = torch.Generator(device=device)
     g.manual_seed(layer_seed(seed, 999))
-    return torch_normal((wl.batch, wl.depth, wl.heads, wl.head_dim), g, dtype, device)
+    return torch_normal((wl.batch, wl.cross_queries, wl.heads, wl.head_dim), g, dtype, device)
