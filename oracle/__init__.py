@@ -16,6 +16,10 @@ This package is a plain, slow, obviously-correct restatement of what the paper
 * ``verify``     -- greedy acceptance of the longest matching root path
                     (Sec. 3, speculative decoding with greedy acceptance;
                     Sec. 5.1, "Experiment design").
+* ``commit``     -- the accepted path's keys and values moved behind the
+                    prefix in every layer's cache, the rest discarded, and the
+                    new length (Sec. 3; Sec. 4.1, the cache kept after a
+                    verification step).
 
 Only the test-suite, ``__graft_entry__.smoke()`` and the ``cpu_baseline`` leg
 of ``bench.py`` may import this package.  The HIP library never calls it and
@@ -28,4 +32,4 @@ causal-attention routine, the paper's own mask formula, closed forms, boundary
 tables and hand-derived golden fixtures).  No function is "parity unpinned".
 """
 
-from . import attention, cape, verify  # noqa: F401
+from . import attention, cape, commit, verify  # noqa: F401
