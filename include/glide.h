@@ -16,6 +16,9 @@
  *   tree_verify        greedy longest-accepted-path selection (Sec. 3;
  *                      Sec. 5.1 "Experiment design": greedy acceptance for
  *                      the CaPE experiments).
+ *   glide_verify_commit  argmax, acceptance and the KV cache commit of the
+ *                      accepted path in every layer (Sec. 3; Sec. 4.1, the
+ *                      cache kept after a verification step).
  *
  * Conventions shared by every call:
  *   - All array arguments are DEVICE pointers to memory the caller owns and
@@ -177,6 +180,43 @@ int glide_argmax_rows(const float* logits, int rows, int V, int32_t* idx_out,
 int tree_verify(const int32_t* target_argmax, const int32_t* cand_tokens,
                 const int32_t* parents, int B, int N, int32_t* accept_len,
                 int32_t* last_node, int32_t* bonus, hipStream_t stream);
+
+/*
+ * glide_verify_commit -- the verification epilogue: the target's greedy
+ * token per tree row, greedy acceptance of the tree, and the commit of the
+ * accepted path to the KV cache (Sec. 3: the accepted proposal tokens plus
+ * one target token extend the prefix; Sec. 4.1: after a verification step
+ * only the accepted tokens' cache rows are kept; Sec. 4.2: a tree candidate
+ * is accepted when its whole root path is).
+ *
+ * With L = seq_lens[b] and the accepted node's root path n_1, ..., n_a
+ * (depths 1..a), every layer's K and V row L + n_d moves to row L + d - 1;
+ * other rows are left as they are.  seq_lens_out[b] = L + a.
+ *
+ *   logits        [B, N + 1, V] float32: row 0 = the target's logits after
+ *                 the prefix, row n + 1 = after tree node n.
+ *   cand_tokens   [B, N] int32 (padding nodes carry -1 and never match).
+ *   parents       [B, N] int32.
+ *   k_caches, v_caches  HOST arrays of `layers` DEVICE pointers, each a
+ *                 [B, H, L_cap, D] cache of `dtype` holding node m's key /
+ *                 value at row L + m (the layout glide_tree_attn reads);
+ *                 updated in place.  0 <= layers <= 128 (0: no commit).
+ *   seq_lens      [B] int32 in; seq_lens_out [B] int32 out (must not be
+ *                 seq_lens: the launch still reads the old lengths).
+ *   target_argmax [B, N + 1] int32 out (as glide_argmax_rows).
+ *   accept_len    [B] int32 out; last_node, bonus [B] and path [B, N]
+ *                 (accepted node at depth d + 1 in slot d, -1 after) int32
+ *                 out, nullable.
+ *   B <= 65535; 1 <= N <= 64; D == 128; L_cap >= N; seq_lens[b] + N <=
+ *   L_cap (clamped into range unless GLIDE_VALIDATE=1).
+ * Two launches (the argmax, then the acceptance and copy); no workspace.
+ */
+int glide_verify_commit(const float* logits, int V, const int32_t* cand_tokens,
+                        const int32_t* parents, int B, int N, void* const* k_caches,
+                        void* const* v_caches, int layers, int H, int D, int L_cap,
+                        int dtype, const int32_t* seq_lens, int32_t* seq_lens_out,
+                        int32_t* target_argmax, int32_t* accept_len, int32_t* last_node,
+                        int32_t* bonus, int32_t* path, hipStream_t stream);
 
 #ifdef __cplusplus
 }

@@ -7,6 +7,8 @@ include/glide.h).  Functions carry the C names:
     cape_expand       confidence-aware proposal expansion into a tree
     glide_argmax_rows the target's greedy token per logits row
     tree_verify       greedy longest-accepted-path selection
+    glide_verify_commit  argmax, acceptance and the KV cache commit of the
+                      accepted path in every layer
 
 PyTorch only provides device memory and streams.
 """
@@ -14,5 +16,5 @@ PyTorch only provides device memory and streams.
 from ._lib import (  # noqa: F401
     CAPE_MAX_K, GLIDE_BF16, GLIDE_EHIP, GLIDE_EINVAL, GLIDE_ERANGE, GLIDE_F32, GLIDE_OK,
     HEAD_DIM, MAX_NODES, MAX_SPLITS, GlideError, attn_workspace, cape_expand,
-    glide_argmax_rows, glide_tree_attn, load, tree_verify,
+    glide_argmax_rows, glide_tree_attn, glide_verify_commit, load, tree_verify,
 )

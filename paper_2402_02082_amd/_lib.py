@@ -56,13 +56,16 @@ def load():
     lib.glide_argmax_rows.argtypes = [P, I, I, P, P]
     lib.tree_verify.restype = I
     lib.tree_verify.argtypes = [P, P, P, I, I, P, P, P, P]
+    lib.glide_verify_commit.restype = I
+    lib.glide_verify_commit.argtypes = [P, I, P, P, I, I, P, P, I, I, I, I, I, P, P, P, P, P, P, P,
+                                        P]
     _lib = lib
     return lib
 
 
 EXPORTED = ["glide_strerror", "glide_last_hip_error", "glide_tree_attn_workspace",
             "glide_tree_attn", "cape_expand_workspace", "cape_expand",
-            "glide_argmax_rows", "tree_verify"]
+            "glide_argmax_rows", "tree_verify", "glide_verify_commit"]
 
 
 def _ptr(t):
@@ -193,4 +196,48 @@ def tree_verify(target_argmax, cand_tokens, parents, accept_len, last_node=None,
                                 _ptr(accept_len), _ptr(last_node), _ptr(bonus),
                                 _stream(stream, cand_tokens.device))
     _check("tree_verify", status)
+    return accept_len
+
+
+def glide_verify_commit(logits, cand_tokens, parents, k_caches, v_caches, seq_lens, seq_lens_out,
+                        target_argmax, accept_len, last_node=None, bonus=None, path=None,
+                        stream=None):
+    """Argmax of every tree row, greedy acceptance and the commit of the
+    accepted path to every layer's K/V cache (in place); see include/glide.h.
+    k_caches, v_caches: sequences of per-layer [B, H, L_cap, D] tensors."""
+    _dev(logits, "logits", torch.float32)
+    _dev(cand_tokens, "cand_tokens", torch.int32)
+    B, N = cand_tokens.shape
+    _need(logits.dim() == 3 and tuple(logits.shape[:2]) == (B, N + 1),
+          "logits must be [B, N + 1, V]")
+    V = logits.shape[2]
+    _dev(parents, "parents", torch.int32)
+    _need(tuple(parents.shape) == (B, N), "parents must be [B, N]")
+    for name, t, shape in (("seq_lens", seq_lens, (B,)), ("seq_lens_out", seq_lens_out, (B,)),
+                           ("target_argmax", target_argmax, (B, N + 1)),
+                           ("accept_len", accept_len, (B,)), ("last_node", last_node, (B,)),
+                           ("bonus", bonus, (B,)), ("path", path, (B, N))):
+        if t is not None or name in ("seq_lens", "seq_lens_out", "target_argmax", "accept_len"):
+            _dev(t, name, torch.int32)
+            _need(tuple(t.shape) == shape, "%s must be %s" % (name, shape))
+    k_caches, v_caches = list(k_caches), list(v_caches)
+    _need(len(k_caches) == len(v_caches), "k_caches and v_caches must have one entry per layer")
+    layers = len(k_caches)
+    H, L_cap, D, dtype = 1, N, HEAD_DIM, GLIDE_BF16
+    if layers:
+        ref = k_caches[0]
+        _need(ref.dtype in (torch.bfloat16, torch.float32), "caches must be bfloat16 or float32")
+        _need(ref.dim() == 4 and ref.shape[0] == B, "caches must be [B, H, L_cap, D]")
+        H, L_cap, D = ref.shape[1], ref.shape[2], ref.shape[3]
+        dtype = GLIDE_BF16 if ref.dtype == torch.bfloat16 else GLIDE_F32
+        for i, t in enumerate(k_caches + v_caches):
+            _dev(t, "cache %d" % i, ref.dtype)
+            _need(t.shape == ref.shape, "every cache must be [B, H, L_cap, D] like the first")
+    kp = (ctypes.c_void_p * max(layers, 1))(*[t.data_ptr() for t in k_caches])
+    vp = (ctypes.c_void_p * max(layers, 1))(*[t.data_ptr() for t in v_caches])
+    status = load().glide_verify_commit(
+        _ptr(logits), V, _ptr(cand_tokens), _ptr(parents), B, N, kp, vp, layers, H, D, L_cap,
+        dtype, _ptr(seq_lens), _ptr(seq_lens_out), _ptr(target_argmax), _ptr(accept_len),
+        _ptr(last_node), _ptr(bonus), _ptr(path), _stream(stream, logits.device))
+    _check("glide_verify_commit", status)
     return accept_len

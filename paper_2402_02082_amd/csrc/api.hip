@@ -164,4 +164,52 @@ int tree_verify(const int32_t* target_argmax, const int32_t* cand_tokens, const 
                                               last_node, bonus, stream));
 }
 
+int glide_verify_commit(const float* logits, int V, const int32_t* cand_tokens, const int32_t* parents,
+                        int B, int N, void* const* k_caches, void* const* v_caches, int layers, int H,
+                        int D, int L_cap, int dtype, const int32_t* seq_lens, int32_t* seq_lens_out,
+                        int32_t* target_argmax, int32_t* accept_len, int32_t* last_node, int32_t* bonus,
+                        int32_t* path, hipStream_t stream) {
+  if (!logits || !cand_tokens || !parents || !seq_lens || !seq_lens_out || !target_argmax ||
+      !accept_len)
+    return GLIDE_EINVAL;
+  if (seq_lens_out == seq_lens) return GLIDE_EINVAL;  // other workgroups still read the lengths
+  if (V < 1 || B < 1 || B > 65535 || N < 1 || N > glide::kMaxNodes) return GLIDE_EINVAL;
+  if ((double)B * (N + 1) * V > 9.0e18) return GLIDE_EINVAL;
+  if (layers < 0 || layers > glide::kMaxLayers) return GLIDE_EINVAL;
+  if (dtype != GLIDE_BF16 && dtype != GLIDE_F32) return GLIDE_EINVAL;
+  if (!tree_attn_sizes_ok(B, N, H, D, L_cap, true)) return GLIDE_EINVAL;
+  if (layers > 0 && (!k_caches || !v_caches)) return GLIDE_EINVAL;
+  glide::CommitArgs a{};
+  for (int l = 0; l < layers; ++l) {
+    if (!k_caches[l] || !v_caches[l]) return GLIDE_EINVAL;
+    a.k[l] = (char*)k_caches[l];
+    a.v[l] = (char*)v_caches[l];
+  }
+  if (validate_enabled()) {
+    int status = GLIDE_OK;
+    std::vector<int32_t> lens, par;
+    if (!fetch_ints(seq_lens, (size_t)B, lens, stream, &status)) return status;
+    for (int b = 0; b < B; ++b)
+      if (lens[b] < 0 || lens[b] > L_cap - N) return GLIDE_ERANGE;
+    if (!fetch_ints(parents, (size_t)B * N, par, stream, &status)) return status;
+    if (!parents_ok(par, B, N)) return GLIDE_ERANGE;
+  }
+  a.target_argmax = target_argmax;
+  a.cand = cand_tokens;
+  a.parents = parents;
+  a.seq_lens = seq_lens;
+  a.seq_lens_out = seq_lens_out;
+  a.accept_len = accept_len;
+  a.last_node = last_node;
+  a.bonus = bonus;
+  a.path = path;
+  a.B = B;
+  a.N = N;
+  a.H = H;
+  a.L_cap = L_cap;
+  a.layers = layers;
+  a.row_bytes = D * (dtype == GLIDE_BF16 ? 2 : 4);
+  return hip_status(glide::launch_verify_commit(logits, V, a, stream));
+}
+
 }  // extern "C"

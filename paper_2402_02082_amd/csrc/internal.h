@@ -48,6 +48,25 @@ hipError_t launch_cape_expand(const float* probs, int B, int gamma, int V, int k
 hipError_t launch_argmax_rows(const float* logits, int rows, int V, int32_t* idx,
                               hipStream_t stream);
 
+// Greedy acceptance plus the cache commit of every layer's K and V.
+constexpr int kMaxLayers = 128;
+struct CommitArgs {
+  int32_t* target_argmax;  // [B, N + 1], written by the argmax launch
+  const int32_t* cand;
+  const int32_t* parents;
+  const int32_t* seq_lens;
+  int32_t* seq_lens_out;
+  int32_t* accept_len;
+  int32_t* last_node;      // nullable
+  int32_t* bonus;          // nullable
+  int32_t* path;           // nullable, [B, N]
+  int B, N, H, L_cap, layers, row_bytes;
+  char* k[kMaxLayers];
+  char* v[kMaxLayers];
+};
+
+hipError_t launch_verify_commit(const float* logits, int V, const CommitArgs& a, hipStream_t stream);
+
 hipError_t launch_tree_verify(const int32_t* target_argmax, const int32_t* cand,
                               const int32_t* parents, int B, int N,
                               int32_t* accept_len, int32_t* last_node,

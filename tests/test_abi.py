@@ -126,3 +126,26 @@ def test_binding_rejects_host_tensors():
     q = torch.zeros(1, 4, 2, 128, dtype=torch.bfloat16)
     with pytest.raises(ValueError):
         glide.glide_tree_attn(q, q, q, torch.zeros(1, dtype=torch.int32), None, q)
+
+
+def _commit(lib, **kw):
+    ptrs = (ctypes.c_void_p * 2)(0x1000, 0x2000)
+    a = dict(logits=FAKE, V=32000, cand=FAKE, par=FAKE, B=1, N=16, kc=ptrs, vc=ptrs, layers=2,
+             H=32, D=128, L_cap=2064, dtype=0, lens=ctypes.c_void_p(0x3000),
+             lens_out=ctypes.c_void_p(0x4000), ta=FAKE, acc=FAKE)
+    a.update(kw)
+    return lib.glide_verify_commit(a["logits"], a["V"], a["cand"], a["par"], a["B"], a["N"],
+                                   a["kc"], a["vc"], a["layers"], a["H"], a["D"], a["L_cap"],
+                                   a["dtype"], a["lens"], a["lens_out"], a["ta"], a["acc"], None,
+                                   None, None, None)
+
+
+@pytest.mark.parametrize("bad", [
+    dict(logits=None), dict(cand=None), dict(par=None), dict(lens=None), dict(lens_out=None),
+    dict(ta=None), dict(acc=None), dict(lens_out=ctypes.c_void_p(0x3000)), dict(V=0), dict(B=0),
+    dict(B=65536), dict(N=0), dict(N=65), dict(layers=-1), dict(layers=129), dict(dtype=2),
+    dict(H=0), dict(D=64), dict(L_cap=15), dict(kc=None), dict(vc=None),
+    dict(kc=(ctypes.c_void_p * 2)(0x1000, None)),
+])
+def test_verify_commit_rejects(lib, bad):
+    assert _commit(lib, **bad) == glide.GLIDE_EINVAL
