@@ -6,11 +6,12 @@ in the order a decoding round runs it:
   1. cape_expand        draft distributions -> expanded proposal tree;
   2. glide_tree_attn    one verification attention launch per target layer,
                         with the tree just built (tree mode);
-  3. glide_argmax_rows  the target's greedy token per tree row;
-  4. tree_verify        accept length, last node and bonus token;
-  5. glide_tree_attn    the GliDe cross-attention of the draft's gamma query
-                        rows into the top target layer's cache (cross mode),
-                        for workloads that have one.
+  3. glide_verify_commit  the target's greedy token per tree row, accept
+                        length, last node and bonus token, and the commit of
+                        the accepted path's K/V rows in every layer;
+  4. glide_tree_attn    the GliDe cross-attention of the draft's query rows
+                        into the top target layer's cache (cross mode), for
+                        workloads that have one.
 Inputs are generated and resident in HBM before timing starts.
 
 Default workload: Vicuna-7B verify step (32 layers x 32 heads, head_dim 128,
@@ -89,6 +90,10 @@ class Step:
         self.acc = torch.empty((B,), dtype=torch.int32, device=dev)
         self.last = torch.empty((B,), dtype=torch.int32, device=dev)
         self.bonus = torch.empty((B,), dtype=torch.int32, device=dev)
+        self.path = torch.empty((B, N), dtype=torch.int32, device=dev)
+        self.seq_out = torch.empty((B,), dtype=torch.int32, device=dev)
+        self.k_caches = [k for _, k, _ in self.layers]
+        self.v_caches = [v for _, _, v in self.layers]
         L_cap = wl.l_cap
         self.ws = glide.attn_workspace(B, N, wl.heads, L_cap, max_splits, dev)
         self.xws = (glide.attn_workspace(B, wl.cross_queries, wl.heads, L_cap, max_splits, dev)
@@ -112,15 +117,29 @@ class Step:
             glide.glide_tree_attn(q, k, v, self.lens, parents, o, max_splits=self.max_splits,
                                   workspace=self.ws)
 
+    def commit(self):
+        """Argmax, acceptance and the cache commit of every layer."""
+        tokens, parents = self.tree()
+        glide.glide_verify_commit(self.logits, tokens, parents, self.k_caches, self.v_caches,
+                                  self.lens, self.seq_out, self.ta, self.acc, self.last,
+                                  self.bonus, self.path)
+
+    def commit_bytes(self):
+        """Algorithmic bytes of one commit: the logits read once, and every
+        moved K/V row of every layer and head read and written once."""
+        wl = self.wl
+        acc, path = self.acc.cpu().numpy(), self.path.cpu().numpy()
+        moved = sum(int(np.sum(path[b, :acc[b]] != np.arange(acc[b]))) for b in range(wl.batch))
+        row = 128 * self.layers[0][1].element_size()
+        return self.logits.numel() * 4 + 2 * 2 * moved * wl.heads * wl.layers * row, moved
+
     def run(self):
         wl = self.wl
         if self.probs is not None:
             glide.cape_expand(self.probs, wl.k, wl.nodes, self.tokens, self.parents, self.n_nodes,
                               workspace=self.cape_ws)
-        tokens, parents = self.tree()
         self.run_verify_layers()
-        glide.glide_argmax_rows(self.logits, self.ta)
-        glide.tree_verify(self.ta, tokens, parents, self.acc, self.last, self.bonus)
+        self.commit()
         if wl.cross:
             _, k, v = self.layers[-1]
             glide.glide_tree_attn(self.cross_q, k, v, self.lens, None, self.cross_out,
@@ -129,17 +148,21 @@ class Step:
 
 def cpu_baseline(step, budget_s=12.0):
     """The float64 oracle on a bounded sample of the same step: the CaPE
-    expansion, argmax and verification in full, then verification-attention
-    layers (all heads) until ~budget_s, then the cross-attention layer.
-    Reported in the metric's unit (attention GB/s) with the BLAS threads used."""
+    expansion and the verification epilogue (argmax, acceptance, commit of
+    every layer's cache) in full, then verification-attention layers (all
+    heads) until ~budget_s, then the cross-attention layer.  Reported in the
+    metric's unit (attention GB/s) with the BLAS threads used."""
     import threadpoolctl
 
     from oracle import attention as OA
     from oracle import cape as OC
-    from oracle import verify as OV
+    from oracle import commit as OCm
 
     wl = step.wl
     f64 = lambda t: t.float().cpu().numpy().astype(np.float64)  # noqa: E731
+    bits = lambda t: t.view(torch.int16 if t.dtype == torch.bfloat16 else torch.int32).cpu().numpy()  # noqa: E731
+    k_bits = [bits(k) for k in step.k_caches]
+    v_bits = [bits(v) for v in step.v_caches]
     with threadpoolctl.threadpool_limits(1):
         t0 = time.perf_counter()
         if wl.tree == "cape":
@@ -147,9 +170,10 @@ def cpu_baseline(step, budget_s=12.0):
         else:
             tokens = step.chain_tokens.cpu().numpy()
             parents = step.chain_parents.cpu().numpy()
-        ta = OV.argmax_rows(step.logits_np)
-        OV.tree_verify(ta, tokens, parents)
+        OCm.verify_commit(step.logits_np, tokens, parents, step.lens_np, k_bits, v_bits)
         t_int = time.perf_counter() - t0
+    del k_bits, v_bits
+    with threadpoolctl.threadpool_limits(1):
         t_attn, nbytes, layers_done = 0.0, 0, 0
         for (q, k, v) in step.layers:
             qh, kh, vh = f64(q), f64(k), f64(v)
@@ -168,7 +192,8 @@ def cpu_baseline(step, budget_s=12.0):
             nbytes += step.cross_bytes
     total = t_attn + t_int
     return {"value": round(nbytes / total / 1e9, 6), "unit": "GB/s", "cores": 1, "kind": "oracle",
-            "sample": "%s: CaPE expansion, argmax and tree verification in full, %d of %d "
+            "sample": "%s: CaPE expansion and the verification epilogue (argmax, acceptance, "
+                      "commit of every layer) in full, %d of %d "
                       "verification-attention layers (all heads)%s, float64 NumPy, %.1f s"
                       % (wl.name, layers_done, wl.layers, " + the cross-attention layer"
                          if wl.cross else "", total)}
@@ -198,11 +223,14 @@ def load_traffic():
 
 def measure(wl, steps, warmup, max_splits):
     """Builds a workload's step, captures it (and its verification layers
-    alone) as HIP graphs, and times both with HIP events around the replays."""
+    alone, and its verification epilogue alone) as HIP graphs, and times
+    them with HIP events around the replays.  Short calls are captured
+    several times per graph so that a replay outlasts the host's cost of
+    launching it; times are per repetition."""
     step = Step(wl, torch.bfloat16, SEED, max_splits)
     torch.cuda.synchronize()
-    # Capture one whole step, and the verification layers alone, as HIP
-    # graphs (the library never allocates, so both replay as captured).
+    rep = max(1, 16 // wl.layers)   # steps / verification passes per graph
+    rep_commit = 16                 # verification epilogues per graph
     side = torch.cuda.Stream()
     side.wait_stream(torch.cuda.current_stream())
     with torch.cuda.stream(side):
@@ -210,35 +238,49 @@ def measure(wl, steps, warmup, max_splits):
             step.run()
     torch.cuda.current_stream().wait_stream(side)
     torch.cuda.synchronize()
-    g_step, g_verify = torch.cuda.CUDAGraph(), torch.cuda.CUDAGraph()
+    g_step, g_verify, g_commit = torch.cuda.CUDAGraph(), torch.cuda.CUDAGraph(), torch.cuda.CUDAGraph()
     with torch.cuda.graph(g_step):
-        step.run()
+        for _ in range(rep):
+            step.run()
     with torch.cuda.graph(g_verify):
-        step.run_verify_layers()
+        for _ in range(rep):
+            step.run_verify_layers()
+    with torch.cuda.graph(g_commit):
+        for _ in range(rep_commit):
+            step.commit()
     torch.cuda.synchronize()
     for _ in range(warmup):
         g_step.replay()
     torch.cuda.synchronize()
 
-    # Timed region 1: K whole steps (graph replays).
-    start, stop = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
-    start.record()
-    for _ in range(steps):
-        g_step.replay()
-    stop.record()
-    torch.cuda.synchronize()
-    ms_step = start.elapsed_time(stop) / steps
-    planted_ok = bool(np.array_equal(step.acc.cpu().numpy(), step.planted))
+    def timed(graph, per):
+        start, stop = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        start.record()
+        for _ in range(steps):
+            graph.replay()
+        stop.record()
+        torch.cuda.synchronize()
+        return start.elapsed_time(stop) / (steps * per)
 
+    # Timed region 1: whole steps.
+    ms_step = timed(g_step, rep)
+    planted_ok = bool(np.array_equal(step.acc.cpu().numpy(), step.planted))
     # Timed region 2: the verification step alone (the L attention calls).
-    start.record()
-    for _ in range(steps):
-        g_verify.replay()
-    stop.record()
-    torch.cuda.synchronize()
-    verify_us = start.elapsed_time(stop) / steps * 1e3
-    del g_step, g_verify
-    return step, {"ms_step": ms_step, "verify_us": verify_us, "planted_ok": planted_ok}
+    verify_us = timed(g_verify, rep) * 1e3
+    # Timed region 3: the verification epilogue alone (argmax, acceptance,
+    # commit of every layer).
+    commit_us = timed(g_commit, rep_commit) * 1e3
+    del g_step, g_verify, g_commit
+    return step, {"ms_step": ms_step, "verify_us": verify_us, "planted_ok": planted_ok,
+                  "commit_us": commit_us, "graph_reps": rep}
+
+
+def commit_record(step, t):
+    nbytes, moved = step.commit_bytes()
+    return {"us": round(t["commit_us"], 2), "bytes": nbytes,
+            "gbps": round(nbytes / (t["commit_us"] * 1e-6) / 1e9, 1),
+            "rows_moved": moved, "layers": step.wl.layers,
+            "launches": "argmax + acceptance/commit"}
 
 
 def other_configs(skip, steps, warmup, max_splits):
@@ -260,7 +302,8 @@ def other_configs(skip, steps, warmup, max_splits):
                     "verify_frac_of_hbm_peak": round(vgbps / HBM_PEAK_GBPS, 4),
                     "ms_per_step": round(t["ms_step"], 4),
                     "step_gbps": round(sbytes / (t["ms_step"] * 1e-3) / 1e9, 1),
-                    "planted_accept_len_ok": t["planted_ok"]})
+                    "planted_accept_len_ok": t["planted_ok"],
+                    "verify_commit": commit_record(step, t)})
         del step
         torch.cuda.empty_cache()
     return out
@@ -360,6 +403,7 @@ def main():
         "verify_step_gbps": round(step.verify_bytes * wl.layers / (verify_us * 1e-6) / 1e9, 2),
         "hbm_frac_of_step": round(value / HBM_PEAK_GBPS, 4),
         "planted_accept_len_ok": planted_ok,
+        "verify_commit": commit_record(step, t),
         "roofline": {"bound": "hbm", "achieved": round(achieved, 2), "peak": HBM_PEAK_GBPS,
                      "unit": "GB/s", "frac": round(achieved / HBM_PEAK_GBPS, 4),
                      "traffic": load_traffic(),
