@@ -16,6 +16,9 @@ This package is a plain, slow, obviously-correct restatement of what the paper
 * ``verify``     -- greedy acceptance of the longest matching root path
                     (Sec. 3, speculative decoding with greedy acceptance;
                     Sec. 5.1, "Experiment design").
+* ``cross_block`` -- the GliDe cross-attention sub-layer with its query and
+                    output projections (Sec. 4.1, the Q^{m,j} and MultiHead
+                    equations).
 * ``commit``     -- the accepted path's keys and values moved behind the
                     prefix in every layer's cache, the rest discarded, and the
                     new length (Sec. 3; Sec. 4.1, the cache kept after a
@@ -32,4 +35,4 @@ causal-attention routine, the paper's own mask formula, closed forms, boundary
 tables and hand-derived golden fixtures).  No function is "parity unpinned".
 """
 
-from . import attention, cape, commit, verify  # noqa: F401
+from . import attention, cape, commit, cross_block, verify  # noqa: F401
