@@ -19,6 +19,10 @@
  *   glide_verify_commit  argmax, acceptance and the KV cache commit of the
  *                      accepted path in every layer (Sec. 3; Sec. 4.1, the
  *                      cache kept after a verification step).
+ *   glide_cross_block  the GliDe cross-attention sub-layer with its query
+ *                      and output projections (Sec. 4.1, Q^{m,j} and
+ *                      MultiHead equations); glide_rows_matmul is its
+ *                      few-row projection.
  *
  * Conventions shared by every call:
  *   - All array arguments are DEVICE pointers to memory the caller owns and
@@ -217,6 +221,41 @@ int glide_verify_commit(const float* logits, int V, const int32_t* cand_tokens,
                         int dtype, const int32_t* seq_lens, int32_t* seq_lens_out,
                         int32_t* target_argmax, int32_t* accept_len, int32_t* last_node,
                         int32_t* bonus, int32_t* path, hipStream_t stream);
+
+/*
+ * glide_rows_matmul -- out[m, n] = sum_k a[m, k] * w_t[n, k], the projection
+ * of a few activation rows by a weight matrix stored one row per output
+ * feature (Sec. 4.1: Q^{m,j} = H^m W_j for every head j, and
+ * Concat(hd_1..hd_h) W^O; w_t is the transpose of the paper's W).
+ *   a   [M, K] bfloat16, 16-byte aligned;  w_t [N, K] bfloat16, 16-byte
+ *       aligned;  out [M, N] of out_dtype (GLIDE_BF16 rounds to nearest
+ *       even, GLIDE_F32 keeps the float32 accumulation).
+ *   M >= 1 (64 rows per launch, more rows take further launches, each
+ *   reading w_t again); 8 <= K <= 2^20 with K % 8 == 0; N >= 1.
+ */
+int glide_rows_matmul(const void* a, const void* w_t, void* out, int M, int K, int N,
+                      int out_dtype, hipStream_t stream);
+
+/*
+ * glide_cross_block -- MultiHead(Q^m, K^l, V^l) = Concat(hd_1..hd_h) W^O with
+ * hd_j = SoftMax(Q^{m,j} (K^{l,j})^T / sqrt(d_k)) V^{l,j} and Q^{m,j} = H^m W_j
+ * (Sec. 4.1): the draft's hidden rows projected into one query per target
+ * head, attended over the target layer's cache (rows [0, seq_lens[b]), as
+ * glide_tree_attn in cross mode) and projected back.  bfloat16 throughout;
+ * the projected queries and the concatenated heads are stored in bfloat16
+ * in the workspace between the three launches.
+ *   hidden [B, Nq, d_D];  wq_t [H*D, d_D] (row j*D + c = column c of W_j);
+ *   k_cache, v_cache [B, H, L_cap, D];  seq_lens [B] int32;
+ *   wo_t [d_D, H*D] (the transpose of W^O);  out [B, Nq, d_D].
+ *   D == 128; 1 <= Nq <= 64; d_D % 8 == 0; scale <= 0 means 1/sqrt(D);
+ *   workspace of glide_cross_block_workspace() bytes, 16-byte aligned,
+ *   needing no initialisation (0 for invalid sizes).
+ */
+size_t glide_cross_block_workspace(int B, int Nq, int d_D, int H, int D, int L_cap);
+int glide_cross_block(const void* hidden, const void* wq_t, const void* k_cache,
+                      const void* v_cache, const int32_t* seq_lens, const void* wo_t, void* out,
+                      int B, int Nq, int d_D, int H, int D, int L_cap, float scale,
+                      void* workspace, size_t ws_bytes, hipStream_t stream);
 
 #ifdef __cplusplus
 }

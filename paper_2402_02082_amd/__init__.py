@@ -9,6 +9,9 @@ include/glide.h).  Functions carry the C names:
     tree_verify       greedy longest-accepted-path selection
     glide_verify_commit  argmax, acceptance and the KV cache commit of the
                       accepted path in every layer
+    glide_cross_block the GliDe cross-attention sub-layer (query projection,
+                      cross attention, output projection)
+    glide_rows_matmul its few-row projection
 
 PyTorch only provides device memory and streams.
 """
@@ -16,5 +19,6 @@ PyTorch only provides device memory and streams.
 from ._lib import (  # noqa: F401
     CAPE_MAX_K, GLIDE_BF16, GLIDE_EHIP, GLIDE_EINVAL, GLIDE_ERANGE, GLIDE_F32, GLIDE_OK,
     HEAD_DIM, MAX_NODES, MAX_SPLITS, GlideError, attn_workspace, cape_expand,
-    glide_argmax_rows, glide_tree_attn, glide_verify_commit, load, tree_verify,
+    cross_block_workspace, glide_argmax_rows, glide_cross_block, glide_rows_matmul,
+    glide_tree_attn, glide_verify_commit, load, tree_verify,
 )

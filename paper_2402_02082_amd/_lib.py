@@ -56,6 +56,12 @@ def load():
     lib.glide_argmax_rows.argtypes = [P, I, I, P, P]
     lib.tree_verify.restype = I
     lib.tree_verify.argtypes = [P, P, P, I, I, P, P, P, P]
+    lib.glide_rows_matmul.restype = I
+    lib.glide_rows_matmul.argtypes = [P, P, P, I, I, I, I, P]
+    lib.glide_cross_block_workspace.restype = Z
+    lib.glide_cross_block_workspace.argtypes = [I, I, I, I, I, I]
+    lib.glide_cross_block.restype = I
+    lib.glide_cross_block.argtypes = [P, P, P, P, P, P, P, I, I, I, I, I, I, F, P, Z, P]
     lib.glide_verify_commit.restype = I
     lib.glide_verify_commit.argtypes = [P, I, P, P, I, I, P, P, I, I, I, I, I, P, P, P, P, P, P, P,
                                         P]
@@ -65,7 +71,8 @@ def load():
 
 EXPORTED = ["glide_strerror", "glide_last_hip_error", "glide_tree_attn_workspace",
             "glide_tree_attn", "cape_expand_workspace", "cape_expand",
-            "glide_argmax_rows", "tree_verify", "glide_verify_commit"]
+            "glide_argmax_rows", "tree_verify", "glide_verify_commit", "glide_rows_matmul",
+            "glide_cross_block_workspace", "glide_cross_block"]
 
 
 def _ptr(t):
@@ -241,3 +248,55 @@ def glide_verify_commit(logits, cand_tokens, parents, k_caches, v_caches, seq_le
         _ptr(last_node), _ptr(bonus), _ptr(path), _stream(stream, logits.device))
     _check("glide_verify_commit", status)
     return accept_len
+
+
+def glide_rows_matmul(a, w_t, out, stream=None):
+    """out[m, n] = sum_k a[m, k] * w_t[n, k]; a [M, K], w_t [N, K] bfloat16,
+    out [M, N] bfloat16 or float32."""
+    _dev(a, "a", torch.bfloat16)
+    _dev(w_t, "w_t", torch.bfloat16)
+    _need(a.dim() == 2 and w_t.dim() == 2 and a.shape[1] == w_t.shape[1],
+          "a must be [M, K] and w_t [N, K]")
+    M, K = a.shape
+    N = w_t.shape[0]
+    _need(out.dtype in (torch.bfloat16, torch.float32), "out must be bfloat16 or float32")
+    _dev(out, "out")
+    _need(tuple(out.shape) == (M, N), "out must be [M, N]")
+    status = load().glide_rows_matmul(_ptr(a), _ptr(w_t), _ptr(out), M, K, N,
+                                      GLIDE_BF16 if out.dtype == torch.bfloat16 else GLIDE_F32,
+                                      _stream(stream, a.device))
+    _check("glide_rows_matmul", status)
+    return out
+
+
+def cross_block_workspace(B, Nq, d_D, H, L_cap, device):
+    need = load().glide_cross_block_workspace(B, Nq, d_D, H, HEAD_DIM, L_cap)
+    _need(need > 0, "unsupported cross-attention block sizes")
+    return torch.empty(need, dtype=torch.uint8, device=device)
+
+
+def glide_cross_block(hidden, wq_t, k_cache, v_cache, seq_lens, wo_t, out, scale=0.0,
+                      workspace=None, stream=None):
+    """The GliDe cross-attention sub-layer: hidden [B, Nq, d_D] -> out [B, Nq, d_D]
+    through the query projection, cross attention over the cache and the
+    output projection (bfloat16).  See include/glide.h."""
+    for name, t in (("hidden", hidden), ("wq_t", wq_t), ("k_cache", k_cache),
+                    ("v_cache", v_cache), ("wo_t", wo_t), ("out", out)):
+        _dev(t, name, torch.bfloat16)
+    _dev(seq_lens, "seq_lens", torch.int32)
+    B, Nq, d_D = hidden.shape
+    _need(k_cache.dim() == 4 and k_cache.shape[0] == B, "k_cache must be [B, H, L_cap, D]")
+    _need(v_cache.shape == k_cache.shape, "v_cache must match k_cache")
+    H, L_cap, D = k_cache.shape[1], k_cache.shape[2], k_cache.shape[3]
+    _need(tuple(wq_t.shape) == (H * D, d_D), "wq_t must be [H*D, d_D]")
+    _need(tuple(wo_t.shape) == (d_D, H * D), "wo_t must be [d_D, H*D]")
+    _need(tuple(out.shape) == (B, Nq, d_D), "out must be [B, Nq, d_D]")
+    _need(seq_lens.shape == (B,), "seq_lens must be [B]")
+    if workspace is None:
+        workspace = cross_block_workspace(B, Nq, d_D, H, L_cap, hidden.device)
+    status = load().glide_cross_block(
+        _ptr(hidden), _ptr(wq_t), _ptr(k_cache), _ptr(v_cache), _ptr(seq_lens), _ptr(wo_t),
+        _ptr(out), B, Nq, d_D, H, D, L_cap, float(scale), _ptr(workspace),
+        workspace.numel() * workspace.element_size(), _stream(stream, hidden.device))
+    _check("glide_cross_block", status)
+    return out

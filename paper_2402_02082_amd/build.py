@@ -13,7 +13,7 @@ ROOT = os.path.dirname(PKG)
 CSRC = os.path.join(PKG, "csrc")
 INCLUDE = os.path.join(ROOT, "include")
 LIB = os.path.join(PKG, "libglide.so")
-SOURCES = ["api.hip", "tree_attn.hip", "cape.hip", "verify.hip", "commit.hip"]
+SOURCES = ["api.hip", "tree_attn.hip", "cape.hip", "verify.hip", "commit.hip", "rows_matmul.hip"]
 
 HIPCC_FLAGS = [
     "--offload-arch=gfx950",

@@ -57,6 +57,58 @@ bool tree_attn_sizes_ok(int B, int N, int H, int D, int L_cap, bool tree) {
   return true;
 }
 
+glide::AttnArgs attn_args(const void* q, const void* k_cache, const void* v_cache,
+                          const int32_t* seq_lens, const int32_t* tree_parents, void* out, int B,
+                          int N, int H, int D, int L_cap, float scale, const glide::AttnPlan& plan,
+                          void* workspace) {
+  glide::AttnArgs a{};
+  a.q = q;
+  a.k = k_cache;
+  a.v = v_cache;
+  a.seq_lens = seq_lens;
+  a.parents = tree_parents;
+  a.out = out;
+  char* ws = (char*)workspace;
+  a.part_o = plan.ws_bytes ? (float*)(ws + plan.part_o_off) : nullptr;
+  a.part_ml = plan.ws_bytes ? (float2*)(ws + plan.part_ml_off) : nullptr;
+  a.B = B;
+  a.N = N;
+  a.H = H;
+  a.L_cap = L_cap;
+  a.chunk = plan.chunk;
+  a.splits = plan.splits;
+  const double sc = scale > 0.f ? (double)scale : 1.0 / sqrt((double)D);
+  a.scale_log2 = (float)(sc * 1.4426950408889634);  // log2(e)
+  return a;
+}
+
+bool aligned16(const void* p) { return ((uintptr_t)p & 15) == 0; }
+
+bool rows_matmul_sizes_ok(int M, int K, int N) {
+  return M >= 1 && N >= 1 && K >= 8 && K % 8 == 0 && K <= glide::kMaxMatmulK;
+}
+
+size_t align256(size_t n) { return (n + 255) & ~(size_t)255; }
+
+// Workspace of the cross-attention block: projected queries, concatenated
+// heads (both bf16 [B, Nq, H, D]) and the attention's split partials.
+struct CrossPlan {
+  glide::AttnPlan attn;
+  size_t q_off, heads_off, attn_off, bytes;
+};
+
+bool cross_block_plan(int B, int Nq, int d_D, int H, int D, int L_cap, CrossPlan* p) {
+  if (!tree_attn_sizes_ok(B, Nq, H, D, L_cap, false)) return false;
+  if (!rows_matmul_sizes_ok(B * Nq, d_D, H * D) || (double)B * Nq > 1.0e9) return false;
+  p->attn = glide::plan_tree_attn(B, Nq, H, L_cap, 0);
+  const size_t rows = align256((size_t)B * Nq * H * D * 2);
+  p->q_off = 0;
+  p->heads_off = rows;
+  p->attn_off = 2 * rows;
+  p->bytes = 2 * rows + p->attn.ws_bytes;
+  return true;
+}
+
 }  // namespace
 
 extern "C" {
@@ -104,24 +156,8 @@ int glide_tree_attn(const void* q, const void* k_cache, const void* v_cache, con
     }
   }
 
-  glide::AttnArgs a{};
-  a.q = q;
-  a.k = k_cache;
-  a.v = v_cache;
-  a.seq_lens = seq_lens;
-  a.parents = tree_parents;
-  a.out = out;
-  char* ws = (char*)workspace;
-  a.part_o = plan.ws_bytes ? (float*)(ws + plan.part_o_off) : nullptr;
-  a.part_ml = plan.ws_bytes ? (float2*)(ws + plan.part_ml_off) : nullptr;
-  a.B = B;
-  a.N = N;
-  a.H = H;
-  a.L_cap = L_cap;
-  a.chunk = plan.chunk;
-  a.splits = plan.splits;
-  const double sc = scale > 0.f ? (double)scale : 1.0 / sqrt((double)D);
-  a.scale_log2 = (float)(sc * 1.4426950408889634);  // log2(e)
+  const glide::AttnArgs a = attn_args(q, k_cache, v_cache, seq_lens, tree_parents, out, B, N, H, D,
+                                      L_cap, scale, plan, workspace);
   return hip_status(glide::launch_tree_attn(a, dtype == GLIDE_BF16, stream));
 }
 
@@ -210,6 +246,50 @@ int glide_verify_commit(const float* logits, int V, const int32_t* cand_tokens, 
   a.layers = layers;
   a.row_bytes = D * (dtype == GLIDE_BF16 ? 2 : 4);
   return hip_status(glide::launch_verify_commit(logits, V, a, stream));
+}
+
+int glide_rows_matmul(const void* a, const void* w_t, void* out, int M, int K, int N, int out_dtype,
+                      hipStream_t stream) {
+  if (!a || !w_t || !out || !aligned16(a) || !aligned16(w_t)) return GLIDE_EINVAL;
+  if (!rows_matmul_sizes_ok(M, K, N)) return GLIDE_EINVAL;
+  if (out_dtype != GLIDE_BF16 && out_dtype != GLIDE_F32) return GLIDE_EINVAL;
+  return hip_status(glide::launch_rows_matmul(a, w_t, out, M, K, N, out_dtype == GLIDE_BF16, stream));
+}
+
+size_t glide_cross_block_workspace(int B, int Nq, int d_D, int H, int D, int L_cap) {
+  CrossPlan p;
+  return cross_block_plan(B, Nq, d_D, H, D, L_cap, &p) ? p.bytes : 0;
+}
+
+int glide_cross_block(const void* hidden, const void* wq_t, const void* k_cache, const void* v_cache,
+                      const int32_t* seq_lens, const void* wo_t, void* out, int B, int Nq, int d_D,
+                      int H, int D, int L_cap, float scale, void* workspace, size_t ws_bytes,
+                      hipStream_t stream) {
+  if (!hidden || !wq_t || !k_cache || !v_cache || !seq_lens || !wo_t || !out || !workspace)
+    return GLIDE_EINVAL;
+  if (!aligned16(hidden) || !aligned16(wq_t) || !aligned16(wo_t) || !aligned16(workspace))
+    return GLIDE_EINVAL;
+  if (!isfinite(scale)) return GLIDE_EINVAL;
+  CrossPlan p;
+  if (!cross_block_plan(B, Nq, d_D, H, D, L_cap, &p) || ws_bytes < p.bytes) return GLIDE_EINVAL;
+  if (validate_enabled()) {
+    int status = GLIDE_OK;
+    std::vector<int32_t> lens;
+    if (!fetch_ints(seq_lens, (size_t)B, lens, stream, &status)) return status;
+    for (int b = 0; b < B; ++b)
+      if (lens[b] < 0 || lens[b] > L_cap) return GLIDE_ERANGE;
+  }
+  char* ws = (char*)workspace;
+  void* q = ws + p.q_off;
+  void* heads = ws + p.heads_off;
+  const int M = B * Nq;
+  hipError_t e = glide::launch_rows_matmul(hidden, wq_t, q, M, d_D, H * D, true, stream);
+  if (e != hipSuccess) return hip_status(e);
+  const glide::AttnArgs a = attn_args(q, k_cache, v_cache, seq_lens, nullptr, heads, B, Nq, H, D,
+                                      L_cap, scale, p.attn, ws + p.attn_off);
+  e = glide::launch_tree_attn(a, true, stream);
+  if (e != hipSuccess) return hip_status(e);
+  return hip_status(glide::launch_rows_matmul(heads, wo_t, out, M, H * D, d_D, true, stream));
 }
 
 }  // extern "C"

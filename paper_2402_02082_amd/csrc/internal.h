@@ -48,6 +48,13 @@ hipError_t launch_cape_expand(const float* probs, int B, int gamma, int V, int k
 hipError_t launch_argmax_rows(const float* logits, int rows, int V, int32_t* idx,
                               hipStream_t stream);
 
+// out[m, n] = sum_k a[m, k] w_t[n, k] (bf16 in, fp32 accumulation); up to
+// kMaxMatmulRows rows per launch, more rows loop.
+constexpr int kMaxMatmulRows = 64;
+constexpr int kMaxMatmulK = 1 << 20;
+hipError_t launch_rows_matmul(const void* a, const void* w_t, void* out, int M, int K, int N,
+                              bool out_bf16, hipStream_t stream);
+
 // Greedy acceptance plus the cache commit of every layer's K and V.
 constexpr int kMaxLayers = 128;
 struct CommitArgs {

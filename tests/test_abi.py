@@ -149,3 +149,43 @@ def _commit(lib, **kw):
 ])
 def test_verify_commit_rejects(lib, bad):
     assert _commit(lib, **bad) == glide.GLIDE_EINVAL
+
+
+@pytest.mark.parametrize("args", [
+    (None, FAKE, FAKE, 5, 4096, 4096, 0), (FAKE, None, FAKE, 5, 4096, 4096, 0),
+    (FAKE, FAKE, None, 5, 4096, 4096, 0), (ctypes.c_void_p(0x1002), FAKE, FAKE, 5, 4096, 4096, 0),
+    (FAKE, ctypes.c_void_p(0x1008), FAKE, 5, 4096, 4096, 0), (FAKE, FAKE, FAKE, 0, 4096, 4096, 0),
+    (FAKE, FAKE, FAKE, 5, 0, 4096, 0), (FAKE, FAKE, FAKE, 5, 12, 4096, 0),
+    (FAKE, FAKE, FAKE, 5, (1 << 20) + 8, 4096, 0), (FAKE, FAKE, FAKE, 5, 4096, 0, 0),
+    (FAKE, FAKE, FAKE, 5, 4096, 4096, 2),
+])
+def test_rows_matmul_rejects(lib, args):
+    assert lib.glide_rows_matmul(*args, None) == glide.GLIDE_EINVAL
+
+
+def test_cross_block_workspace(lib):
+    rows = 1 * 5 * 32 * 128 * 2                      # bf16 [B, Nq, H, D], 256-aligned already
+    attn = lib.glide_tree_attn_workspace(1, 5, 32, 128, 2064, 0)
+    assert lib.glide_cross_block_workspace(1, 5, 4096, 32, 128, 2064) == 2 * rows + attn
+    assert lib.glide_cross_block_workspace(1, 5, 4096, 32, 64, 2064) == 0
+    assert lib.glide_cross_block_workspace(1, 65, 4096, 32, 128, 2064) == 0
+    assert lib.glide_cross_block_workspace(1, 5, 4100, 32, 128, 2064) == 0
+
+
+def _xblock(lib, **kw):
+    a = dict(h=FAKE, wq=FAKE, k=FAKE, v=FAKE, lens=FAKE, wo=FAKE, out=FAKE, B=1, Nq=5, dD=4096,
+             H=32, D=128, L_cap=2064, scale=0.0, ws=FAKE, ws_bytes=1 << 30)
+    a.update(kw)
+    return lib.glide_cross_block(a["h"], a["wq"], a["k"], a["v"], a["lens"], a["wo"], a["out"],
+                                 a["B"], a["Nq"], a["dD"], a["H"], a["D"], a["L_cap"], a["scale"],
+                                 a["ws"], a["ws_bytes"], None)
+
+
+@pytest.mark.parametrize("bad", [
+    dict(h=None), dict(wq=None), dict(k=None), dict(v=None), dict(lens=None), dict(wo=None),
+    dict(out=None), dict(ws=None), dict(h=ctypes.c_void_p(0x1004)), dict(ws=ctypes.c_void_p(0x1001)),
+    dict(B=0), dict(Nq=0), dict(Nq=65), dict(dD=12), dict(H=0), dict(D=64), dict(L_cap=0),
+    dict(scale=float("nan")), dict(ws_bytes=1024),
+])
+def test_cross_block_rejects(lib, bad):
+    assert _xblock(lib, **bad) == glide.GLIDE_EINVAL

@@ -1,0 +1,105 @@
+"""GPU parity of glide_rows_matmul and glide_cross_block against the float64
+oracle.  rows_matmul with float32 output: max-abs error <= 1e-4 (the
+accumulation error of 4096 float32 products of O(1) values is ~1e-5).  A
+bfloat16 output carries one rounding to 8 significant bits, up to 2^-8 of
+the value (0.016 for values in [4, 8)), so the bound for bfloat16-stored
+results is 1e-2 + 2^-8 |reference|.  The block stores its projected queries
+and concatenated heads in bfloat16, so the oracle rounds the same two
+intermediates (store=bfloat16) and the same bound applies to its output."""
+
+import numpy as np
+import pytest
+import torch
+
+import paper_2402_02082_amd as glide
+from oracle import cross_block as OX
+from synth import workloads as W
+from tests.gpu_common import BF16_TOL, require_gpu, say, to64
+
+pytestmark = pytest.mark.gpu
+
+F32_OUT_TOL = 1e-4
+
+
+def bf16_ok(got, want):
+    """Every element within 1e-2 + 2^-8 |want|; returns the worst excess."""
+    return float(np.max(np.abs(got - want) - (BF16_TOL + 2.0 ** -8 * np.abs(want))))
+
+
+def _bf16(shape, seed, scale=1.0):
+    g = torch.Generator().manual_seed(seed)
+    return (torch.randn(shape, generator=g) * scale).to(torch.bfloat16)
+
+
+@pytest.mark.parametrize("M,K,N", [(1, 8, 1), (5, 4096, 4096), (16, 4096, 4096), (17, 512, 100),
+                                   (64, 1024, 333), (130, 256, 48), (3, 4104, 16), (5, 96, 4096)])
+@pytest.mark.parametrize("out_dtype", [torch.float32, torch.bfloat16])
+def test_rows_matmul(M, K, N, out_dtype):
+    require_gpu()
+    say("rows_matmul", dict(M=M, K=K, N=N, out=str(out_dtype)))
+    a = _bf16((M, K), 1 + M)
+    w_t = _bf16((N, K), 2 + N, 1.0 / np.sqrt(K))
+    out = torch.full((M, N), float("nan"), dtype=out_dtype, device="cuda")
+    glide.glide_rows_matmul(a.cuda(), w_t.cuda(), out)
+    torch.cuda.synchronize()
+    want = OX.rows_matmul(to64(a), to64(w_t))
+    if out_dtype == torch.float32:
+        err = float(np.abs(to64(out) - want).max())
+        assert err <= F32_OUT_TOL, err
+    else:
+        excess = bf16_ok(to64(out), want)
+        assert excess <= 0, excess
+
+
+def _block_case(seed, B, Nq, H, d_D, L_cap, lens):
+    dev = torch.device("cuda")
+    hidden = _bf16((B, Nq, d_D), seed).to(dev)
+    wq_t = _bf16((H * 128, d_D), seed + 1, 1.0 / np.sqrt(d_D)).to(dev)
+    wo_t = _bf16((d_D, H * 128), seed + 2, 1.0 / np.sqrt(H * 128)).to(dev)
+    k = _bf16((B, H, L_cap, 128), seed + 3).to(dev)
+    v = _bf16((B, H, L_cap, 128), seed + 4).to(dev)
+    return hidden, wq_t, k, v, torch.tensor(lens, dtype=torch.int32, device=dev), wo_t
+
+
+@pytest.mark.parametrize("B,Nq,H,d_D,L_cap,lens", [
+    (1, 5, 2, 256, 300, [300]),
+    (3, 7, 4, 520, 700, [0, 1, 699]),
+    (2, 16, 3, 384, 2100, [2050, 37]),
+])
+def test_cross_block_small(B, Nq, H, d_D, L_cap, lens):
+    require_gpu()
+    say("cross_block", dict(B=B, Nq=Nq, H=H, d_D=d_D, L_cap=L_cap, lens=lens))
+    hidden, wq_t, k, v, sl, wo_t = _block_case(7 + B, B, Nq, H, d_D, L_cap, lens)
+    out = torch.full_like(hidden, float("nan"))
+    glide.glide_cross_block(hidden, wq_t, k, v, sl, wo_t, out)
+    torch.cuda.synchronize()
+    want = OX.cross_block(to64(hidden), to64(wq_t), to64(k), to64(v), lens, to64(wo_t),
+                          store=torch.bfloat16)
+    excess = bf16_ok(to64(out), want)
+    assert excess <= 0, excess
+
+
+@pytest.mark.parametrize("cfg", [2, 5])
+def test_cross_block_workload(cfg):
+    """The workload's cross layer as a full block (d_D = 4096 = H * D), on the
+    seeded cache; sequences sampled for the oracle (first and last)."""
+    require_gpu()
+    wl = W.WORKLOADS[cfg]
+    dev = torch.device("cuda")
+    lens_np = W.prefix_lengths(wl, 2)
+    lens = torch.from_numpy(lens_np).to(dev)
+    _, k, v = W.attention_layer(wl, 2, wl.layers - 1, torch.bfloat16, dev)
+    d_D = wl.heads * 128
+    hidden = _bf16((wl.batch, wl.cross_queries, d_D), 31).to(dev)
+    wq_t = _bf16((d_D, d_D), 32, 1.0 / np.sqrt(d_D)).to(dev)
+    wo_t = _bf16((d_D, d_D), 33, 1.0 / np.sqrt(d_D)).to(dev)
+    out = torch.full_like(hidden, float("nan"))
+    say("cross_block workload", wl.name)
+    glide.glide_cross_block(hidden, wq_t, k, v, lens, wo_t, out)
+    torch.cuda.synchronize()
+    for b in sorted({0, wl.batch - 1}):
+        L = int(lens_np[b])
+        want = OX.cross_block(to64(hidden[b:b + 1]), to64(wq_t), to64(k[b:b + 1, :, :L]),
+                              to64(v[b:b + 1, :, :L]), [L], to64(wo_t), store=torch.bfloat16)
+        excess = bf16_ok(to64(out[b:b + 1]), want)
+        assert excess <= 0, (b, excess)
