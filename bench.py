@@ -202,7 +202,7 @@ def cpu_baseline(step, budget_s=12.0):
 def kernel_source_hash():
     import hashlib
     src = b"".join(open(os.path.join(ROOT, "paper_2402_02082_amd", "csrc", n), "rb").read()
-                   for n in ("tree_attn.hip", "internal.h"))
+                   for n in ("tree_attn.hip", "attn.h"))
     return hashlib.sha256(src).hexdigest()[:16]
 
 
@@ -283,6 +283,63 @@ def commit_record(step, t):
             "launches": "argmax + acceptance/commit"}
 
 
+def cross_block_record(step, steps, copies=8):
+    """The GliDe cross-attention block (query projection, cross attention,
+    output projection) at d_D = H * 128 on the workload's caches: `copies`
+    distinct weight sets and layers per graph, so the working set (over
+    256 MB) cannot be served from the last-level cache; also the query
+    projection alone.  Random bf16 weights scaled 1/sqrt(d_D)."""
+    wl = step.wl
+    dev = step.dev
+    B, Nq, H = wl.batch, wl.cross_queries, wl.heads
+    d_D = H * 128
+    copies = min(copies, wl.layers)
+    g = torch.Generator(device=dev)
+    g.manual_seed(SEED)
+    mk = lambda *shape: (torch.randn(shape, generator=g, device=dev) / np.sqrt(shape[-1])).to(torch.bfloat16)  # noqa: E731
+    hidden = torch.randn((B, Nq, d_D), generator=g, device=dev).to(torch.bfloat16)
+    wq = [mk(H * 128, d_D) for _ in range(copies)]
+    wo = [mk(d_D, H * 128) for _ in range(copies)]
+    outs = [torch.empty_like(hidden) for _ in range(copies)]
+    q_out = torch.empty((B * Nq, H * 128), dtype=torch.bfloat16, device=dev)
+    ws = glide.cross_block_workspace(B, Nq, d_D, H, wl.l_cap, dev)
+
+    def blocks():
+        for i in range(copies):
+            _, k, v = step.layers[i]
+            glide.glide_cross_block(hidden, wq[i], k, v, step.lens, wo[i], outs[i], workspace=ws)
+
+    def projections():
+        for i in range(copies):
+            glide.glide_rows_matmul(hidden.view(B * Nq, d_D), wq[i], q_out)
+
+    res = {}
+    for name, fn in (("block", blocks), ("projection", projections)):
+        fn()
+        torch.cuda.synchronize()
+        graph = torch.cuda.CUDAGraph()
+        with torch.cuda.graph(graph):
+            fn()
+        graph.replay()
+        torch.cuda.synchronize()
+        start, stop = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        start.record()
+        for _ in range(steps):
+            graph.replay()
+        stop.record()
+        torch.cuda.synchronize()
+        res[name] = start.elapsed_time(stop) * 1e3 / (steps * copies)
+        del graph
+    act = B * Nq * d_D * 2
+    proj_bytes = H * 128 * d_D * 2 + act + B * Nq * H * 128 * 2
+    block_bytes = 2 * proj_bytes + step.cross_bytes
+    return {"us": round(res["block"], 2), "bytes": block_bytes,
+            "gbps": round(block_bytes / (res["block"] * 1e-6) / 1e9, 1),
+            "projection_us": round(res["projection"], 2), "projection_bytes": proj_bytes,
+            "projection_gbps": round(proj_bytes / (res["projection"] * 1e-6) / 1e9, 1),
+            "d_D": d_D, "query_rows": B * Nq, "copies_per_graph": copies}
+
+
 def other_configs(skip, steps, warmup, max_splits):
     """The verification step and the whole step of every other workload,
     measured as the headline one (same seed, graphs, events)."""
@@ -303,7 +360,8 @@ def other_configs(skip, steps, warmup, max_splits):
                     "ms_per_step": round(t["ms_step"], 4),
                     "step_gbps": round(sbytes / (t["ms_step"] * 1e-3) / 1e9, 1),
                     "planted_accept_len_ok": t["planted_ok"],
-                    "verify_commit": commit_record(step, t)})
+                    "verify_commit": commit_record(step, t),
+                    "cross_block": cross_block_record(step, steps) if wl.cross else None})
         del step
         torch.cuda.empty_cache()
     return out
@@ -404,6 +462,7 @@ def main():
         "hbm_frac_of_step": round(value / HBM_PEAK_GBPS, 4),
         "planted_accept_len_ok": planted_ok,
         "verify_commit": commit_record(step, t),
+        "cross_block": cross_block_record(step, args.steps) if wl.cross else None,
         "roofline": {"bound": "hbm", "achieved": round(achieved, 2), "peak": HBM_PEAK_GBPS,
                      "unit": "GB/s", "frac": round(achieved / HBM_PEAK_GBPS, 4),
                      "traffic": load_traffic(),

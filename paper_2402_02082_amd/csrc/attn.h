@@ -1,0 +1,42 @@
+// Interface of the attention kernels (tree_attn.hip) to the C ABI.
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stddef.h>
+#include <stdint.h>
+
+namespace glide {
+
+constexpr int kHeadDim = 128;
+constexpr int kMaxNodes = 64;
+constexpr int kMaxSplits = 64;
+constexpr int kNumCU = 256;        // MI355X compute units (split heuristic)
+constexpr int kChunkQuantum = 32;  // split boundaries are multiples of this
+constexpr int kMinChunk = 128;     // smallest split the automatic plan makes
+
+// How the keys of one (sequence, head) are divided between workgroups.
+struct AttnPlan {
+  int splits;       // workgroups per (sequence, head)
+  int chunk;        // keys per workgroup (multiple of kChunkQuantum)
+  size_t ws_bytes;  // workspace for the partial states (0 if splits == 1)
+  size_t part_o_off, part_ml_off;
+};
+
+AttnPlan plan_tree_attn(int B, int N, int H, int L_cap, int max_splits);
+
+struct AttnArgs {
+  const void* q;
+  const void* k;
+  const void* v;
+  const int32_t* seq_lens;
+  const int32_t* parents;  // nullptr: cross mode
+  void* out;
+  float* part_o;           // [B, H, splits, N, D]
+  float2* part_ml;         // [B, H, splits, N] (running max in log2 units, sum)
+  int B, N, H, L_cap, chunk, splits;
+  float scale_log2;        // softmax scale * log2(e)
+};
+
+hipError_t launch_tree_attn(const AttnArgs& a, bool bf16, hipStream_t stream);
+
+}  // namespace glide

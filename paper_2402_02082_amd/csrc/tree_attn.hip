@@ -39,7 +39,7 @@
 
 #include <type_traits>
 
-#include "internal.h"
+#include "attn.h"
 
 namespace glide {
 namespace {
