@@ -19,6 +19,10 @@
  *   glide_verify_commit  argmax, acceptance and the KV cache commit of the
  *                      accepted path in every layer (Sec. 3; Sec. 4.1, the
  *                      cache kept after a verification step).
+ *   spec_sample_verify chain verification with speculative sampling (Sec. 3;
+ *                      Sec. 5.1, the GliDe-only experiments), and
+ *                      glide_expected_speedup, the expected-speedup model
+ *                      (Sec. 5.1, Metrics).
  *   glide_cross_block  the GliDe cross-attention sub-layer with its query
  *                      and output projections (Sec. 4.1, Q^{m,j} and
  *                      MultiHead equations); glide_rows_matmul is its
@@ -256,6 +260,36 @@ int glide_cross_block(const void* hidden, const void* wq_t, const void* k_cache,
                       const void* v_cache, const int32_t* seq_lens, const void* wo_t, void* out,
                       int B, int Nq, int d_D, int H, int D, int L_cap, float scale,
                       void* workspace, size_t ws_bytes, hipStream_t stream);
+
+/*
+ * spec_sample_verify -- verification of a gamma-token draft chain with
+ * speculative sampling (Sec. 3: the accepted tokens plus one target token
+ * extend the prefix, and the emitted tokens follow the target's sampling
+ * distribution; Sec. 5.1: gamma = 5 chains in the GliDe-only experiments).
+ * Token x_i is accepted when uniforms[b, i-1] * p_D(x_i) < p_T(x_i) (float32);
+ * at the first rejection, at row j, next_token is drawn from max(0, p_T_j -
+ * p_D_j); if all are accepted it is drawn from p_T row gamma.  Draws use
+ * uniforms[b, gamma] by inverse CDF over the fixed-point weights
+ * floor(p * 2^32): with W their sum, the token is the first whose running
+ * weight exceeds floor(u * W) (a residual of weight 0 falls back to the
+ * target row; a target row of weight 0 gives token 0).
+ *   draft_tokens [B, gamma] int32 in [0, V) (clamped);  draft_probs
+ *   [B, gamma, V] and target_probs [B, gamma + 1, V] float32 (row i of the
+ *   target follows draft token i; row 0 follows the prefix);  uniforms
+ *   [B, gamma + 1] float32 in [0, 1);  accept_len, next_token [B] int32 out.
+ *   1 <= gamma <= 64; 1 <= V <= 2^20.
+ */
+int spec_sample_verify(const int32_t* draft_tokens, const float* draft_probs,
+                       const float* target_probs, const float* uniforms, int B, int gamma,
+                       int V, int32_t* accept_len, int32_t* next_token, hipStream_t stream);
+
+/*
+ * glide_expected_speedup -- E(Spd) = (1 - alpha^(gamma+1)) /
+ * ((1 - alpha)(gamma c + 1)) for acceptance rate alpha in [0, 1], proposal
+ * length gamma >= 1 and cost coefficient c >= 0 (Sec. 5.1, Metrics); NaN
+ * for arguments outside those ranges.  Host function, no GPU work.
+ */
+double glide_expected_speedup(double alpha, int gamma, double c);
 
 #ifdef __cplusplus
 }

@@ -12,6 +12,8 @@ include/glide.h).  Functions carry the C names:
     glide_cross_block the GliDe cross-attention sub-layer (query projection,
                       cross attention, output projection)
     glide_rows_matmul its few-row projection
+    spec_sample_verify  chain verification with speculative sampling
+    glide_expected_speedup  the expected-speedup model
 
 PyTorch only provides device memory and streams.
 """
@@ -20,5 +22,6 @@ from ._lib import (  # noqa: F401
     CAPE_MAX_K, GLIDE_BF16, GLIDE_EHIP, GLIDE_EINVAL, GLIDE_ERANGE, GLIDE_F32, GLIDE_OK,
     HEAD_DIM, MAX_NODES, MAX_SPLITS, GlideError, attn_workspace, cape_expand,
     cross_block_workspace, glide_argmax_rows, glide_cross_block, glide_rows_matmul,
-    glide_tree_attn, glide_verify_commit, load, tree_verify,
+    glide_expected_speedup, glide_tree_attn, glide_verify_commit, load, spec_sample_verify,
+    tree_verify,
 )

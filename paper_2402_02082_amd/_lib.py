@@ -62,6 +62,10 @@ def load():
     lib.glide_cross_block_workspace.argtypes = [I, I, I, I, I, I]
     lib.glide_cross_block.restype = I
     lib.glide_cross_block.argtypes = [P, P, P, P, P, P, P, I, I, I, I, I, I, F, P, Z, P]
+    lib.spec_sample_verify.restype = I
+    lib.spec_sample_verify.argtypes = [P, P, P, P, I, I, I, P, P, P]
+    lib.glide_expected_speedup.restype = ctypes.c_double
+    lib.glide_expected_speedup.argtypes = [ctypes.c_double, I, ctypes.c_double]
     lib.glide_verify_commit.restype = I
     lib.glide_verify_commit.argtypes = [P, I, P, P, I, I, P, P, I, I, I, I, I, P, P, P, P, P, P, P,
                                         P]
@@ -72,7 +76,8 @@ def load():
 EXPORTED = ["glide_strerror", "glide_last_hip_error", "glide_tree_attn_workspace",
             "glide_tree_attn", "cape_expand_workspace", "cape_expand",
             "glide_argmax_rows", "tree_verify", "glide_verify_commit", "glide_rows_matmul",
-            "glide_cross_block_workspace", "glide_cross_block"]
+            "glide_cross_block_workspace", "glide_cross_block", "spec_sample_verify",
+            "glide_expected_speedup"]
 
 
 def _ptr(t):
@@ -300,3 +305,31 @@ def glide_cross_block(hidden, wq_t, k_cache, v_cache, seq_lens, wo_t, out, scale
         workspace.numel() * workspace.element_size(), _stream(stream, hidden.device))
     _check("glide_cross_block", status)
     return out
+
+
+def spec_sample_verify(draft_tokens, draft_probs, target_probs, uniforms, accept_len, next_token,
+                       stream=None):
+    """Speculative-sampling verification of draft chains; see include/glide.h."""
+    _dev(draft_tokens, "draft_tokens", torch.int32)
+    B, gamma = draft_tokens.shape
+    _dev(draft_probs, "draft_probs", torch.float32)
+    _need(draft_probs.dim() == 3 and tuple(draft_probs.shape[:2]) == (B, gamma),
+          "draft_probs must be [B, gamma, V]")
+    V = draft_probs.shape[2]
+    _dev(target_probs, "target_probs", torch.float32)
+    _need(tuple(target_probs.shape) == (B, gamma + 1, V), "target_probs must be [B, gamma + 1, V]")
+    _dev(uniforms, "uniforms", torch.float32)
+    _need(tuple(uniforms.shape) == (B, gamma + 1), "uniforms must be [B, gamma + 1]")
+    for name, t in (("accept_len", accept_len), ("next_token", next_token)):
+        _dev(t, name, torch.int32)
+        _need(tuple(t.shape) == (B,), "%s must be [B]" % name)
+    status = load().spec_sample_verify(_ptr(draft_tokens), _ptr(draft_probs), _ptr(target_probs),
+                                       _ptr(uniforms), B, gamma, V, _ptr(accept_len),
+                                       _ptr(next_token), _stream(stream, draft_tokens.device))
+    _check("spec_sample_verify", status)
+    return accept_len, next_token
+
+
+def glide_expected_speedup(alpha, gamma, c):
+    """E(Spd) = (1 - alpha^(gamma+1)) / ((1 - alpha)(gamma c + 1))."""
+    return load().glide_expected_speedup(float(alpha), int(gamma), float(c))

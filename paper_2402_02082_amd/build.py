@@ -13,7 +13,8 @@ ROOT = os.path.dirname(PKG)
 CSRC = os.path.join(PKG, "csrc")
 INCLUDE = os.path.join(ROOT, "include")
 LIB = os.path.join(PKG, "libglide.so")
-SOURCES = ["api.hip", "tree_attn.hip", "cape.hip", "verify.hip", "commit.hip", "rows_matmul.hip"]
+SOURCES = ["api.hip", "tree_attn.hip", "cape.hip", "verify.hip", "commit.hip", "rows_matmul.hip",
+           "spec_sampling.hip"]
 
 HIPCC_FLAGS = [
     "--offload-arch=gfx950",

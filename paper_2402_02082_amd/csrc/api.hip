@@ -292,4 +292,22 @@ int glide_cross_block(const void* hidden, const void* wq_t, const void* k_cache,
   return hip_status(glide::launch_rows_matmul(heads, wo_t, out, M, H * D, d_D, true, stream));
 }
 
+int spec_sample_verify(const int32_t* draft_tokens, const float* draft_probs, const float* target_probs,
+                       const float* uniforms, int B, int gamma, int V, int32_t* accept_len,
+                       int32_t* next_token, hipStream_t stream) {
+  if (!draft_tokens || !draft_probs || !target_probs || !uniforms || !accept_len || !next_token)
+    return GLIDE_EINVAL;
+  if (B < 1 || gamma < 1 || gamma > glide::kMaxSpecGamma || V < 1 || V > glide::kMaxSpecVocab)
+    return GLIDE_EINVAL;
+  if ((double)B * (gamma + 1) * V > 9.0e18) return GLIDE_EINVAL;
+  return hip_status(glide::launch_spec_sample(draft_tokens, draft_probs, target_probs, uniforms, B, gamma,
+                                              V, accept_len, next_token, stream));
+}
+
+double glide_expected_speedup(double alpha, int gamma, double c) {
+  if (!(alpha >= 0.0 && alpha <= 1.0) || gamma < 1 || !(c >= 0.0)) return NAN;
+  if (alpha == 1.0) return (gamma + 1) / (gamma * c + 1.0);
+  return (1.0 - pow(alpha, gamma + 1)) / ((1.0 - alpha) * (gamma * c + 1.0));
+}
+
 }  // extern "C"

@@ -25,6 +25,12 @@ constexpr int kMaxMatmulK = 1 << 20;
 hipError_t launch_rows_matmul(const void* a, const void* w_t, void* out, int M, int K, int N,
                               bool out_bf16, hipStream_t stream);
 
+hipError_t launch_spec_sample(const int32_t* draft_tokens, const float* p_draft, const float* p_target,
+                              const float* uniforms, int B, int gamma, int V, int32_t* accept_len,
+                              int32_t* next_token, hipStream_t stream);
+constexpr int kMaxSpecGamma = 64;
+constexpr int kMaxSpecVocab = 1 << 20;
+
 // Greedy acceptance plus the cache commit of every layer's K and V.
 constexpr int kMaxLayers = 128;
 struct CommitArgs {

@@ -189,3 +189,31 @@ def _xblock(lib, **kw):
 ])
 def test_cross_block_rejects(lib, bad):
     assert _xblock(lib, **bad) == glide.GLIDE_EINVAL
+
+
+@pytest.mark.parametrize("args", [
+    (None, FAKE, FAKE, FAKE, 1, 5, 32000, FAKE, FAKE), (FAKE, None, FAKE, FAKE, 1, 5, 32000, FAKE, FAKE),
+    (FAKE, FAKE, None, FAKE, 1, 5, 32000, FAKE, FAKE), (FAKE, FAKE, FAKE, None, 1, 5, 32000, FAKE, FAKE),
+    (FAKE, FAKE, FAKE, FAKE, 1, 5, 32000, None, FAKE), (FAKE, FAKE, FAKE, FAKE, 1, 5, 32000, FAKE, None),
+    (FAKE, FAKE, FAKE, FAKE, 0, 5, 32000, FAKE, FAKE), (FAKE, FAKE, FAKE, FAKE, 1, 0, 32000, FAKE, FAKE),
+    (FAKE, FAKE, FAKE, FAKE, 1, 65, 32000, FAKE, FAKE), (FAKE, FAKE, FAKE, FAKE, 1, 5, 0, FAKE, FAKE),
+    (FAKE, FAKE, FAKE, FAKE, 1, 5, (1 << 20) + 1, FAKE, FAKE),
+])
+def test_spec_sample_rejects(lib, args):
+    assert lib.spec_sample_verify(*args, None) == glide.GLIDE_EINVAL
+
+
+def test_expected_speedup_host_function():
+    """The library's host-side E(Spd) against the oracle and Table 1."""
+    import json
+    import math
+    from oracle import spec_sampling as S
+    g = json.load(open(os.path.join(ROOT, "tests", "golden", "table1_expected_speedup.json")))
+    for r in g["rows"]:
+        for a, e in zip(r["acc"], r["spd"]):
+            v = glide.glide_expected_speedup(a / 100.0, g["gamma"], r["cost"] / 100.0)
+            assert abs(v - S.expected_speedup(a / 100.0, g["gamma"], r["cost"] / 100.0)) < 1e-12
+            assert abs(v - e) <= 0.01
+    assert glide.glide_expected_speedup(1.0, 5, 0.1) == pytest.approx(6 / 1.5)
+    for bad in ((-0.1, 5, 0.1), (1.1, 5, 0.1), (0.5, 0, 0.1), (0.5, 5, -1.0)):
+        assert math.isnan(glide.glide_expected_speedup(*bad))
