@@ -340,6 +340,66 @@ def cross_block_record(step, steps, copies=8):
             "d_D": d_D, "query_rows": B * Nq, "copies_per_graph": copies}
 
 
+def spec_sampling_record(steps, gamma=5, V=32000):
+    """Chain verification with speculative sampling (gamma = 5, the GliDe-only
+    experiments' setting) for batch 1 and 16: seeded Dirichlet(0.3) draft
+    rows, target rows blended from them and noise, uniforms as inputs; 16
+    calls per graph (the call is launch-sized)."""
+    dev = torch.device("cuda")
+    rng = np.random.default_rng(SEED)
+    out = {}
+    for B in (1, 16):
+        pd = rng.dirichlet(np.full(V, 0.3), size=(B, gamma)).astype(np.float32)
+        noise = rng.dirichlet(np.full(V, 0.3), size=(B, gamma + 1)).astype(np.float32)
+        pt = noise.copy()
+        pt[:, :gamma] = 0.7 * pd + 0.3 * noise[:, :gamma]
+        tokens = pd.argmax(axis=2).astype(np.int32)
+        u = rng.random((B, gamma + 1)).astype(np.float32)
+        args = [torch.from_numpy(a).to(dev) for a in (tokens, pd, pt, u)]
+        acc = torch.empty((B,), dtype=torch.int32, device=dev)
+        tok = torch.empty((B,), dtype=torch.int32, device=dev)
+        reps = 16
+        glide.spec_sample_verify(*args, acc, tok)
+        torch.cuda.synchronize()
+        graph = torch.cuda.CUDAGraph()
+        with torch.cuda.graph(graph):
+            for _ in range(reps):
+                glide.spec_sample_verify(*args, acc, tok)
+        graph.replay()
+        torch.cuda.synchronize()
+        start, stop = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        start.record()
+        for _ in range(steps):
+            graph.replay()
+        stop.record()
+        torch.cuda.synchronize()
+        us = start.elapsed_time(stop) * 1e3 / (steps * reps)
+        # one draw row (the residual reads the draft row as well) per sequence
+        nbytes = B * (2 * V * 4 + gamma * 12 + (gamma + 1) * 4)
+        out["batch_%d" % B] = {"us": round(us, 2), "bytes": nbytes,
+                               "gbps": round(nbytes / (us * 1e-6) / 1e9, 1),
+                               "mean_accept_len": float(acc.float().mean().item())}
+        del graph
+    out.update({"gamma": gamma, "vocab": V})
+    return out
+
+
+def speedup_model(verify_us, cross_block):
+    """E(Spd) = (1 - a^(g+1)) / ((1 - a)(g c + 1)) at gamma = 5 with GliDe's
+    acceptance rate on Vicuna-7B / GSM8K (Table 1: 64.8 %), once with the
+    paper's cost coefficient (6.7 %) and once with an attention-only proxy
+    measured here: one cross-attention block (a draft step's cross layer) over
+    one verification step's attention."""
+    alpha, gamma, c_paper = 0.648, 5, 0.067
+    rec = {"alpha": alpha, "gamma": gamma, "c_paper": c_paper,
+           "expected_speedup_paper_c": round(glide.glide_expected_speedup(alpha, gamma, c_paper), 4)}
+    if cross_block:
+        c = cross_block["us"] / verify_us
+        rec["c_attention_proxy"] = round(c, 4)
+        rec["expected_speedup_proxy_c"] = round(glide.glide_expected_speedup(alpha, gamma, c), 4)
+    return rec
+
+
 def other_configs(skip, steps, warmup, max_splits):
     """The verification step and the whole step of every other workload,
     measured as the headline one (same seed, graphs, events)."""
@@ -463,6 +523,7 @@ def main():
         "planted_accept_len_ok": planted_ok,
         "verify_commit": commit_record(step, t),
         "cross_block": cross_block_record(step, args.steps) if wl.cross else None,
+        "spec_sampling": spec_sampling_record(args.steps),
         "roofline": {"bound": "hbm", "achieved": round(achieved, 2), "peak": HBM_PEAK_GBPS,
                      "unit": "GB/s", "frac": round(achieved / HBM_PEAK_GBPS, 4),
                      "traffic": load_traffic(),
@@ -473,6 +534,7 @@ def main():
                      "timing": "HIP events around graph replays of the verification "
                                "step's calls, divided by the call count"},
     }
+    rec["speedup_model"] = speedup_model(verify_us, rec["cross_block"])
     if not args.no_cpu_baseline:
         rec["cpu_baseline"] = cpu_baseline(step)
     if not args.headline_only:
