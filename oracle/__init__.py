@@ -22,6 +22,8 @@ This package is a plain, slow, obviously-correct restatement of what the paper
 * ``spec_sampling`` -- chain verification with speculative sampling (Sec. 3;
                     Sec. 5.1, the GliDe-only experiments) and the expected
                     speedup model (Sec. 5.1, Metrics).
+* ``block_attention`` -- the block-wise masked cross-attention of draft
+                    training (Sec. 4.1, "Block-wise Attention Mask").
 * ``commit``     -- the accepted path's keys and values moved behind the
                     prefix in every layer's cache, the rest discarded, and the
                     new length (Sec. 3; Sec. 4.1, the cache kept after a
@@ -38,4 +40,4 @@ causal-attention routine, the paper's own mask formula, closed forms, boundary
 tables and hand-derived golden fixtures).  No function is "parity unpinned".
 """
 
-from . import attention, cape, commit, cross_block, spec_sampling, verify  # noqa: F401
+from . import attention, block_attention, cape, commit, cross_block, spec_sampling, verify  # noqa: F401
