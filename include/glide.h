@@ -23,6 +23,8 @@
  *                      Sec. 5.1, the GliDe-only experiments), and
  *                      glide_expected_speedup, the expected-speedup model
  *                      (Sec. 5.1, Metrics).
+ *   glide_block_attn   the block-wise masked cross attention of draft
+ *                      training (Sec. 4.1, "Block-wise Attention Mask").
  *   glide_cross_block  the GliDe cross-attention sub-layer with its query
  *                      and output projections (Sec. 4.1, Q^{m,j} and
  *                      MultiHead equations); glide_rows_matmul is its
@@ -282,6 +284,21 @@ int glide_cross_block(const void* hidden, const void* wq_t, const void* k_cache,
 int spec_sample_verify(const int32_t* draft_tokens, const float* draft_probs,
                        const float* target_probs, const float* uniforms, int B, int gamma,
                        int V, int32_t* accept_len, int32_t* next_token, hipStream_t stream);
+
+/*
+ * glide_block_attn -- the cross attention of draft training under the
+ * block-wise mask (Sec. 4.1, "Block-wise Attention Mask"): with positions cut
+ * into blocks of `block` tokens, the query at position p attends to the
+ * target's keys and values of the positions k with block(p) > block(k),
+ * i.e. [0, block * floor(p / block)); a query of the first block sees none
+ * and gets zeros.  bfloat16 in and out, float32 accumulation.
+ *   q   [B, T, H, D] (the draft's projected queries of a training sequence);
+ *   k_cache, v_cache [B, H, L_cap, D] holding positions 0 .. T - 1;
+ *   out [B, T, H, D].  D == 128; 1 <= T <= L_cap; block >= 1; B <= 65535;
+ *   scale <= 0 means 1/sqrt(D).
+ */
+int glide_block_attn(const void* q, const void* k_cache, const void* v_cache, void* out, int B,
+                     int T, int H, int D, int L_cap, int block, float scale, hipStream_t stream);
 
 /*
  * glide_expected_speedup -- E(Spd) = (1 - alpha^(gamma+1)) /

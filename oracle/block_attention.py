@@ -32,8 +32,9 @@ def visible_keys(j, L):
     return [k for k in range(L * block_of(j, L)) if block_of(j, L) > block_of(k, L)]
 
 
-def block_attention(q, k_cache, v_cache, T, L, scale=None):
-    """out[b, j, h] = attention of q[b, j, h] over k_cache[b, h, visible_keys(j)]."""
+def block_attention(q, k_cache, v_cache, T, L, scale=None, positions=None):
+    """out[b, j, h] = attention of q[b, j, h] over k_cache[b, h, visible_keys(j)],
+    for every position j or only those listed (others stay zero)."""
     q = np.asarray(q, dtype=np.float64)
     B, _, H, D = q.shape
     sc = 1.0 / np.sqrt(D) if scale is None else float(scale)
@@ -42,7 +43,7 @@ def block_attention(q, k_cache, v_cache, T, L, scale=None):
         for h in range(H):
             kh = np.asarray(k_cache[b, h], dtype=np.float64)
             vh = np.asarray(v_cache[b, h], dtype=np.float64)
-            for j in range(T):
+            for j in (range(T) if positions is None else positions):
                 keys = visible_keys(j, L)
                 out[b, j, h] = OA.attention_rows(q[b, j:j + 1, h], kh[keys], vh[keys], sc)[0]
     return out

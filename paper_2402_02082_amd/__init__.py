@@ -12,6 +12,7 @@ include/glide.h).  Functions carry the C names:
     glide_cross_block the GliDe cross-attention sub-layer (query projection,
                       cross attention, output projection)
     glide_rows_matmul its few-row projection
+    glide_block_attn  the block-masked cross attention of draft training
     spec_sample_verify  chain verification with speculative sampling
     glide_expected_speedup  the expected-speedup model
 
@@ -21,7 +22,8 @@ PyTorch only provides device memory and streams.
 from ._lib import (  # noqa: F401
     CAPE_MAX_K, GLIDE_BF16, GLIDE_EHIP, GLIDE_EINVAL, GLIDE_ERANGE, GLIDE_F32, GLIDE_OK,
     HEAD_DIM, MAX_NODES, MAX_SPLITS, GlideError, attn_workspace, cape_expand,
-    cross_block_workspace, glide_argmax_rows, glide_cross_block, glide_rows_matmul,
+    cross_block_workspace, glide_argmax_rows, glide_block_attn, glide_cross_block,
+    glide_rows_matmul,
     glide_expected_speedup, glide_tree_attn, glide_verify_commit, load, spec_sample_verify,
     tree_verify,
 )

@@ -62,6 +62,8 @@ def load():
     lib.glide_cross_block_workspace.argtypes = [I, I, I, I, I, I]
     lib.glide_cross_block.restype = I
     lib.glide_cross_block.argtypes = [P, P, P, P, P, P, P, I, I, I, I, I, I, F, P, Z, P]
+    lib.glide_block_attn.restype = I
+    lib.glide_block_attn.argtypes = [P, P, P, P, I, I, I, I, I, I, F, P]
     lib.spec_sample_verify.restype = I
     lib.spec_sample_verify.argtypes = [P, P, P, P, I, I, I, P, P, P]
     lib.glide_expected_speedup.restype = ctypes.c_double
@@ -76,7 +78,8 @@ def load():
 EXPORTED = ["glide_strerror", "glide_last_hip_error", "glide_tree_attn_workspace",
             "glide_tree_attn", "cape_expand_workspace", "cape_expand",
             "glide_argmax_rows", "tree_verify", "glide_verify_commit", "glide_rows_matmul",
-            "glide_cross_block_workspace", "glide_cross_block", "spec_sample_verify",
+            "glide_cross_block_workspace", "glide_cross_block", "glide_block_attn",
+            "spec_sample_verify",
             "glide_expected_speedup"]
 
 
@@ -333,3 +336,20 @@ def spec_sample_verify(draft_tokens, draft_probs, target_probs, uniforms, accept
 def glide_expected_speedup(alpha, gamma, c):
     """E(Spd) = (1 - alpha^(gamma+1)) / ((1 - alpha)(gamma c + 1))."""
     return load().glide_expected_speedup(float(alpha), int(gamma), float(c))
+
+
+def glide_block_attn(q, k_cache, v_cache, out, block, scale=0.0, stream=None):
+    """Block-masked training cross attention: q [B, T, H, D] over the cache's
+    positions [0, block * floor(p / block)); bfloat16.  See include/glide.h."""
+    for name, t in (("q", q), ("k_cache", k_cache), ("v_cache", v_cache), ("out", out)):
+        _dev(t, name, torch.bfloat16)
+    B, T, H, D = q.shape
+    _need(k_cache.dim() == 4 and k_cache.shape[:2] == (B, H) and k_cache.shape[3] == D,
+          "k_cache must be [B, H, L_cap, D]")
+    _need(v_cache.shape == k_cache.shape, "v_cache must match k_cache")
+    _need(out.shape == q.shape, "out must match q")
+    status = load().glide_block_attn(_ptr(q), _ptr(k_cache), _ptr(v_cache), _ptr(out), B, T, H, D,
+                                     k_cache.shape[2], int(block), float(scale),
+                                     _stream(stream, q.device))
+    _check("glide_block_attn", status)
+    return out

@@ -292,6 +292,28 @@ int glide_cross_block(const void* hidden, const void* wq_t, const void* k_cache,
   return hip_status(glide::launch_rows_matmul(heads, wo_t, out, M, H * D, d_D, true, stream));
 }
 
+int glide_block_attn(const void* q, const void* k_cache, const void* v_cache, void* out, int B, int T,
+                     int H, int D, int L_cap, int block, float scale, hipStream_t stream) {
+  if (!q || !k_cache || !v_cache || !out) return GLIDE_EINVAL;
+  if (B < 1 || B > 65535 || H < 1 || T < 1 || T > L_cap || D != glide::kHeadDim || block < 1)
+    return GLIDE_EINVAL;
+  if ((T + 63) / 64 > 65535 || !isfinite(scale)) return GLIDE_EINVAL;
+  if ((double)B * H * (double)L_cap * D > 9.0e18 || (double)B * T * H * D > 9.0e18) return GLIDE_EINVAL;
+  glide::BlockAttnArgs a{};
+  a.q = q;
+  a.k = k_cache;
+  a.v = v_cache;
+  a.out = out;
+  a.B = B;
+  a.T = T;
+  a.H = H;
+  a.L_cap = L_cap;
+  a.block = block;
+  const double sc = scale > 0.f ? (double)scale : 1.0 / sqrt((double)D);
+  a.scale_log2 = (float)(sc * 1.4426950408889634);  // log2(e)
+  return hip_status(glide::launch_block_attn(a, stream));
+}
+
 int spec_sample_verify(const int32_t* draft_tokens, const float* draft_probs, const float* target_probs,
                        const float* uniforms, int B, int gamma, int V, int32_t* accept_len,
                        int32_t* next_token, hipStream_t stream) {

@@ -39,4 +39,17 @@ struct AttnArgs {
 
 hipError_t launch_tree_attn(const AttnArgs& a, bool bf16, hipStream_t stream);
 
+// Block-masked cross attention of draft training: query position p attends
+// to key positions [0, block * floor(p / block)).
+struct BlockAttnArgs {
+  const void* q;    // [B, T, H, D] bf16
+  const void* k;    // [B, H, L_cap, D] bf16
+  const void* v;
+  void* out;        // [B, T, H, D] bf16
+  int B, T, H, L_cap, block;
+  float scale_log2;
+};
+
+hipError_t launch_block_attn(const BlockAttnArgs& a, hipStream_t stream);
+
 }  // namespace glide

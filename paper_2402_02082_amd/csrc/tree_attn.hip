@@ -851,6 +851,96 @@ __global__ __launch_bounds__(kThreads) void tree_attn_combine(AttnArgs args) {
 constexpr int kSharedLds4 = 65536;
 constexpr int kSharedLds2 = 65536;
 
+
+// ---------------------------------------------------------------------------
+// Block-masked cross attention of draft training (Sec. 4.1, "Block-wise
+// Attention Mask"): the query at position p sees the target's keys of the
+// earlier blocks, [0, block * floor(p / block)).  One workgroup per (head,
+// sequence, 64 query positions), one wave per 16-position tile, keys streamed
+// through the same LDS ring as the shared-step kernel, tiles with the most
+// keys first.  The mask is the cross-mode step's own: each lane (query) passes
+// its limit as the prefix length, which the step compares per key.
+// ---------------------------------------------------------------------------
+__global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(2)))
+void block_attn_kernel(BlockAttnArgs args) {
+  constexpr int kStages = kSharedLds4 / kStepBytes;
+  constexpr int kStepInstr = kStepBytes / 1024 / kWaves;
+  __shared__ __attribute__((aligned(1024))) char ring[kSharedLds4];
+
+  const int h = blockIdx.x, b = blockIdx.y;
+  const int p0 = (gridDim.z - 1 - blockIdx.z) * 64;   // most keys first
+  const int tid = threadIdx.x, lane = tid & 63;
+  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+  const int c = lane & 15, g = lane >> 4;
+  const int T = args.T, H = args.H, Lcap = args.L_cap, blk = args.block;
+
+  const int p_last = min(p0 + 63, T - 1);
+  const int k_end = blk * (p_last / blk);            // the workgroup's largest limit
+  const int steps = (k_end + 31) / 32;
+  const int p = p0 + 16 * wave + c;
+  const bool tile_live = p0 + 16 * wave < T;
+  const int my_limit = p < T ? blk * (p / blk) : 0;  // keys [0, my_limit) are visible
+  const uint64_t anc[1] = {0};
+
+  const size_t head_off = ((size_t)b * H + h) * (size_t)Lcap * kD;
+  const char* kslab = (const char*)((const uint16_t*)args.k + head_off);
+  const char* vslab = (const char*)((const uint16_t*)args.v + head_off);
+  Bf16Path::QFrag qf[1];
+  load_q<Bf16Path>(qf[0], (const uint16_t*)args.q + (((size_t)b * T + min(p, T - 1)) * H + h) * kD,
+                   p < T, g);
+
+  const int dma_row = 4 * wave + (lane >> 4);
+  const int dma_off = dma_row * 256 + 16 * ((lane & 15) ^ (dma_row & 15));
+  auto issue_step = [&](int t) {
+    char* stage = ring + (t % kStages) * kStepBytes;
+    const int j0 = 32 * t;
+#pragma unroll
+    for (int k = 0; k < kStepInstr; ++k) {
+      const int m = k / 2, hi = k & 1;
+      const __amdgpu_buffer_rsrc_t rs = step_rsrc(m ? vslab : kslab, j0, k_end, 256);
+      char* dst = stage + m * (kStepBytes / 2) + (wave + 4 * hi) * 1024;
+      __builtin_amdgcn_raw_ptr_buffer_load_lds(rs, (lds_ptr_t)dst, 16, dma_off + 4096 * hi, 0, 0,
+                                               kStream);
+    }
+  };
+#pragma unroll
+  for (int t = 0; t < kStages - 1; ++t) issue_step(t);
+
+  SoftmaxState sm[1];
+  sm[0].m = neg_inf();
+  sm[0].l = 0.f;
+  f32x4_t acc[1][8];
+#pragma unroll
+  for (int t = 0; t < 8; ++t) acc[0][t] = f32x4_t{0.f, 0.f, 0.f, 0.f};
+
+  for (int t = 0; t < steps; ++t) {
+    ring_wait_and_meet<(kStages - 2) * kStepInstr>();
+    issue_step(t + kStages - 1);
+    const int j0 = 32 * t;
+    if (tile_live) {
+      Bf16Path::KV f;
+      read_step(f, ring + (t % kStages) * kStepBytes, c, g);
+      if (j0 + 32 > k_end) {
+#pragma unroll
+        for (int i = 0; i < 8; ++i)
+          if (j0 + Bf16Path::key_slot(g, i) >= k_end) f.v[i] = u32x4_t{0, 0, 0, 0};
+      }
+      step<1, false>(f, qf, sm, acc, j0, my_limit, k_end, 64, anc, args.scale_log2, g);
+    }
+  }
+  asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
+  if (!tile_live) return;
+  const float L = sum_across_groups(sm[0].l);
+  const float inv = (L > 0.f) ? 1.f / L : 0.f;
+#pragma unroll
+  for (int r = 0; r < 4; ++r) {
+    float o[8];
+#pragma unroll
+    for (int t = 0; t < 8; ++t) o[t] = acc[0][t][r] * inv;
+    if (p < T) store_row8((uint16_t*)args.out + (((size_t)b * T + p) * H + h) * kD + 32 * g + 8 * r, o);
+  }
+}
+
 template <class P, bool TREE>
 hipError_t launch_nt(const AttnArgs& a, hipStream_t stream) {
   // Heads vary fastest and splits slowest: workgroups are handed to the XCDs
@@ -923,6 +1013,12 @@ AttnPlan plan_tree_attn(int B, int N, int H, int L_cap, int max_splits) {
   p.part_o_off = (units * sizeof(float2) + 255) & ~(size_t)255;
   p.ws_bytes = p.part_o_off + units * kHeadDim * sizeof(float);
   return p;
+}
+
+hipError_t launch_block_attn(const BlockAttnArgs& a, hipStream_t stream) {
+  const dim3 grid(a.H, a.B, (a.T + 63) / 64), block(kThreads);
+  hipLaunchKernelGGL(block_attn_kernel, grid, block, 0, stream, a);
+  return hipGetLastError();
 }
 
 hipError_t launch_tree_attn(const AttnArgs& a, bool bf16, hipStream_t stream) {

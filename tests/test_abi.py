@@ -217,3 +217,19 @@ def test_expected_speedup_host_function():
     assert glide.glide_expected_speedup(1.0, 5, 0.1) == pytest.approx(6 / 1.5)
     for bad in ((-0.1, 5, 0.1), (1.1, 5, 0.1), (0.5, 0, 0.1), (0.5, 5, -1.0)):
         assert math.isnan(glide.glide_expected_speedup(*bad))
+
+
+def _blk(lib, **kw):
+    a = dict(q=FAKE, k=FAKE, v=FAKE, out=FAKE, B=4, T=2048, H=32, D=128, L_cap=2048, block=5,
+             scale=0.0)
+    a.update(kw)
+    return lib.glide_block_attn(a["q"], a["k"], a["v"], a["out"], a["B"], a["T"], a["H"], a["D"],
+                                a["L_cap"], a["block"], a["scale"], None)
+
+
+@pytest.mark.parametrize("bad", [
+    dict(q=None), dict(k=None), dict(v=None), dict(out=None), dict(B=0), dict(B=65536), dict(T=0),
+    dict(T=2049), dict(H=0), dict(D=64), dict(block=0), dict(scale=float("inf")),
+])
+def test_block_attn_rejects(lib, bad):
+    assert _blk(lib, **bad) == glide.GLIDE_EINVAL

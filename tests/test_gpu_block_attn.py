@@ -1,0 +1,50 @@
+"""GPU parity of glide_block_attn (the block-masked cross attention of draft
+training) against the float64 oracle: max-abs error <= 1e-2 (bf16 inputs,
+float32 accumulation, outputs averages of N(0, 1) values)."""
+
+import numpy as np
+import pytest
+import torch
+
+import paper_2402_02082_amd as glide
+from oracle import block_attention as OB
+from tests.gpu_common import BF16_TOL, require_gpu, say, to64
+
+pytestmark = pytest.mark.gpu
+
+
+def _run(seed, B, T, H, L_cap, block, positions=None):
+    g = torch.Generator().manual_seed(seed)
+    q = torch.randn((B, T, H, 128), generator=g).to(torch.bfloat16)
+    k = torch.randn((B, H, L_cap, 128), generator=g).to(torch.bfloat16)
+    v = torch.randn((B, H, L_cap, 128), generator=g).to(torch.bfloat16)
+    out = torch.full((B, T, H, 128), float("nan"), dtype=torch.bfloat16, device="cuda")
+    glide.glide_block_attn(q.cuda(), k.cuda(), v.cuda(), out, block)
+    torch.cuda.synchronize()
+    want = OB.block_attention(to64(q), to64(k), to64(v), T, block, positions=positions)
+    got = to64(out)
+    rows = slice(None) if positions is None else positions
+    return float(np.abs(got[:, rows] - want[:, rows]).max()), got
+
+
+@pytest.mark.parametrize("B,T,H,L_cap,block", [
+    (2, 37, 3, 40, 5), (1, 64, 2, 64, 1), (1, 200, 2, 210, 64), (1, 130, 1, 130, 100),
+    (3, 1, 2, 8, 5), (1, 20, 2, 20, 20), (2, 129, 2, 129, 7),
+])
+def test_small(B, T, H, L_cap, block):
+    require_gpu()
+    say("block_attn", dict(B=B, T=T, H=H, L_cap=L_cap, block=block))
+    err, got = _run(B * 100 + T + block, B, T, H, L_cap, block)
+    assert err <= BF16_TOL, err
+    assert np.all(got[:, :min(block, T)] == 0)   # the first block sees no key
+
+
+def test_training_shape_sampled():
+    """A training-length sequence (T = 2048, blocks of 5): sampled positions
+    at block edges, early and late."""
+    require_gpu()
+    T = 2048
+    pos = sorted({0, 4, 5, 9, 10, 63, 64, 65, 511, 512, 1000, 1024, 2043, 2044, 2045, 2047})
+    say("block_attn training shape", dict(T=T, positions=len(pos)))
+    err, _ = _run(7, 2, T, 4, T, 5, positions=pos)
+    assert err <= BF16_TOL, err
