@@ -384,6 +384,47 @@ def spec_sampling_record(steps, gamma=5, V=32000):
     return out
 
 
+def block_attention_record(steps, B=4, T=2048, H=32, block=5, copies=4):
+    """The block-masked cross attention of draft training at a 7B-head
+    training shape (4 sequences of 2048 positions, blocks of 5): `copies`
+    distinct inputs per graph (1 GB, beyond the last-level cache).  Bound:
+    MFMA (4 * 128 flops per visible key per query and head)."""
+    dev = torch.device("cuda")
+    g = torch.Generator(device=dev)
+    g.manual_seed(SEED)
+    mk = lambda *shape: torch.randn(shape, generator=g, device=dev).to(torch.bfloat16)  # noqa: E731
+    qs = [mk(B, T, H, 128) for _ in range(copies)]
+    ks = [mk(B, H, T, 128) for _ in range(copies)]
+    vs = [mk(B, H, T, 128) for _ in range(copies)]
+    outs = [torch.empty_like(q) for q in qs]
+
+    def fn():
+        for i in range(copies):
+            glide.glide_block_attn(qs[i], ks[i], vs[i], outs[i], block)
+    fn()
+    torch.cuda.synchronize()
+    graph = torch.cuda.CUDAGraph()
+    with torch.cuda.graph(graph):
+        fn()
+    graph.replay()
+    torch.cuda.synchronize()
+    start, stop = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    start.record()
+    for _ in range(steps):
+        graph.replay()
+    stop.record()
+    torch.cuda.synchronize()
+    us = start.elapsed_time(stop) * 1e3 / (steps * copies)
+    flops = B * H * sum(4 * 128 * block * (p // block) for p in range(T))
+    nbytes = 2 * B * T * H * 128 * 2 + 2 * B * H * T * 128 * 2
+    del graph, qs, ks, vs, outs
+    torch.cuda.empty_cache()
+    return {"us": round(us, 1), "flops": flops, "tflops": round(flops / (us * 1e-6) / 1e12, 1),
+            "frac_of_bf16_mfma_peak": round(flops / (us * 1e-6) / 2.5e15, 4),
+            "bytes": nbytes, "gbps": round(nbytes / (us * 1e-6) / 1e9, 1),
+            "shape": {"batch": B, "positions": T, "heads": H, "block": block}}
+
+
 def speedup_model(verify_us, cross_block):
     """E(Spd) = (1 - a^(g+1)) / ((1 - a)(g c + 1)) at gamma = 5 with GliDe's
     acceptance rate on Vicuna-7B / GSM8K (Table 1: 64.8 %), once with the
@@ -524,6 +565,7 @@ def main():
         "verify_commit": commit_record(step, t),
         "cross_block": cross_block_record(step, args.steps) if wl.cross else None,
         "spec_sampling": spec_sampling_record(args.steps),
+        "block_attention": block_attention_record(max(3, min(args.steps, 10))),
         "roofline": {"bound": "hbm", "achieved": round(achieved, 2), "peak": HBM_PEAK_GBPS,
                      "unit": "GB/s", "frac": round(achieved / HBM_PEAK_GBPS, 4),
                      "traffic": load_traffic(),
