@@ -789,13 +789,13 @@ void tree_attn_shared_kernel(AttnArgs args) {
 // Merges the split partial states of every (sequence, head) whose keys were
 // divided, in a fixed split order (the result does not depend on timing).
 // One wave per output row (sequence, query, head); each lane owns two head
-// dims and requests kBatch splits' partials at a time.
+// dims and requests kBatch splits' partials at a time (the plan's split
+// count, up to 8, so no request is a repeat).
 constexpr int kCombineRows = kWaves;  // rows per workgroup
 
-template <class P>
+template <class P, int kBatch>
 __global__ __launch_bounds__(kThreads) void tree_attn_combine(AttnArgs args) {
   typedef typename P::elem_t elem_t;
-  constexpr int kBatch = 8;
   const int N = args.N, H = args.H, Lcap = args.L_cap;
   const int row = blockIdx.x * kCombineRows + (threadIdx.x >> 6);  // (b, n, h) in out order
   const int lane = threadIdx.x & 63;
@@ -961,8 +961,13 @@ hipError_t launch_nt(const AttnArgs& a, hipStream_t stream) {
   hipError_t e = hipGetLastError();
   if (e != hipSuccess || a.splits == 1) return e;
   const int rows = a.B * a.N * a.H;
-  hipLaunchKernelGGL((tree_attn_combine<P>), dim3((rows + kCombineRows - 1) / kCombineRows), block, 0,
-                     stream, a);
+  const dim3 cgrid((rows + kCombineRows - 1) / kCombineRows);
+  if (a.splits <= 2)
+    hipLaunchKernelGGL((tree_attn_combine<P, 2>), cgrid, block, 0, stream, a);
+  else if (a.splits <= 4)
+    hipLaunchKernelGGL((tree_attn_combine<P, 4>), cgrid, block, 0, stream, a);
+  else
+    hipLaunchKernelGGL((tree_attn_combine<P, 8>), cgrid, block, 0, stream, a);
   return hipGetLastError();
 }
 
