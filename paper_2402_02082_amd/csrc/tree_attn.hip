@@ -532,56 +532,57 @@ void tree_attn_kernel(AttnArgs args) {
 #pragma unroll
   for (int nt = 0; nt < NT; ++nt) sm[nt].l = sum_across_groups(sm[nt].l);
 
-  // Merge the waves of each query group through LDS (lane-major stores and
-  // loads: conflict free).  Wave 0 of each group finishes the group's tiles.
-  constexpr int kSlots = QG * (kWpg - 1) * NT;
-  __shared__ float lds_o[kSlots * 8 * 4 * 64];
-  __shared__ float lds_m[kSlots * 64];
-  __shared__ float lds_l[kSlots * 64];
-  if (wig > 0) {
+  // Merge the waves of each query group through LDS.  Every wave publishes
+  // its (max, sum) and its O^T accumulators, then finishes 4 / kWpg of the
+  // four dim blocks r (d = 32 g + 8 r + t) of the group's tiles from all
+  // the group's states, so the merge and the stores are shared out instead
+  // of left to one wave.  Lane-major float4 layout: conflict-free 16-byte
+  // LDS accesses.  States are combined in wave order (results do not depend
+  // on which wave finishes a block).
+  constexpr int kRPerWave = 4 / kWpg;
+  __shared__ f32x4_t lds_o[QG][kWpg][NT][4][2][64];
+  __shared__ float lds_m[QG][kWpg][NT][64];
+  __shared__ float lds_l[QG][kWpg][NT][64];
 #pragma unroll
-    for (int nt = 0; nt < NT; ++nt) {
-      const int slot = (qg * (kWpg - 1) + wig - 1) * NT + nt;
-      lds_m[slot * 64 + lane] = sm[nt].m;
-      lds_l[slot * 64 + lane] = sm[nt].l;
+  for (int nt = 0; nt < NT; ++nt) {
+    lds_m[qg][wig][nt][lane] = sm[nt].m;
+    lds_l[qg][wig][nt][lane] = sm[nt].l;
 #pragma unroll
-      for (int t = 0; t < 8; ++t)
-#pragma unroll
-        for (int r = 0; r < 4; ++r) lds_o[((slot * 8 + t) * 4 + r) * 64 + lane] = acc[nt][t][r];
+    for (int r = 0; r < 4; ++r) {
+      lds_o[qg][wig][nt][r][0][lane] = f32x4_t{acc[nt][0][r], acc[nt][1][r], acc[nt][2][r], acc[nt][3][r]};
+      lds_o[qg][wig][nt][r][1][lane] = f32x4_t{acc[nt][4][r], acc[nt][5][r], acc[nt][6][r], acc[nt][7][r]};
     }
   }
   __syncthreads();
-  if (wig != 0) return;
 
   const size_t part_base = (((size_t)b * H + h) * args.splits + s) * N;
 #pragma unroll
   for (int nt = 0; nt < NT; ++nt) {
     float mw[kWpg], fw[kWpg];
-    mw[0] = sm[nt].m;
 #pragma unroll
-    for (int w = 1; w < kWpg; ++w) mw[w] = lds_m[((qg * (kWpg - 1) + w - 1) * NT + nt) * 64 + lane];
+    for (int w = 0; w < kWpg; ++w) mw[w] = lds_m[qg][w][nt][lane];
     float M = mw[0];
 #pragma unroll
     for (int w = 1; w < kWpg; ++w) M = fmaxf(M, mw[w]);
 #pragma unroll
     for (int w = 0; w < kWpg; ++w) fw[w] = (M == neg_inf()) ? 0.f : fast_exp2(mw[w] - M);
-    float L = fw[0] * sm[nt].l;
+    float L = fw[0] * lds_l[qg][0][nt][lane];
 #pragma unroll
-    for (int w = 1; w < kWpg; ++w) L += fw[w] * lds_l[((qg * (kWpg - 1) + w - 1) * NT + nt) * 64 + lane];
+    for (int w = 1; w < kWpg; ++w) L += fw[w] * lds_l[qg][w][nt][lane];
 
     const int n = 16 * (qg * NT + nt) + c;
     const float inv = (nsplit == 1) ? ((L > 0.f) ? 1.f / L : 0.f) : 1.f;
 #pragma unroll
-    for (int r = 0; r < 4; ++r) {
-      float o[8];
+    for (int i = 0; i < kRPerWave; ++i) {
+      const int r = wig * kRPerWave + i;
+      f32x4_t lo4 = fw[0] * lds_o[qg][0][nt][r][0][lane], hi4 = fw[0] * lds_o[qg][0][nt][r][1][lane];
 #pragma unroll
-      for (int t = 0; t < 8; ++t) {
-        float v = fw[0] * acc[nt][t][r];
-#pragma unroll
-        for (int w = 1; w < kWpg; ++w)
-          v += fw[w] * lds_o[((((qg * (kWpg - 1) + w - 1) * NT + nt) * 8 + t) * 4 + r) * 64 + lane];
-        o[t] = v * inv;
+      for (int w = 1; w < kWpg; ++w) {
+        lo4 += fw[w] * lds_o[qg][w][nt][r][0][lane];
+        hi4 += fw[w] * lds_o[qg][w][nt][r][1][lane];
       }
+      const float o[8] = {lo4[0] * inv, lo4[1] * inv, lo4[2] * inv, lo4[3] * inv,
+                          hi4[0] * inv, hi4[1] * inv, hi4[2] * inv, hi4[3] * inv};
       if (n < N) {
         const int d = 32 * g + 8 * r;
         if (nsplit == 1)
@@ -590,7 +591,7 @@ void tree_attn_kernel(AttnArgs args) {
           store_row8(args.part_o + (part_base + n) * kD + d, o);
       }
     }
-    if (nsplit > 1 && n < N && g == 0) args.part_ml[part_base + n] = make_float2(M, L);
+    if (nsplit > 1 && n < N && g == 0 && wig == 0) args.part_ml[part_base + n] = make_float2(M, L);
   }
 }
 
