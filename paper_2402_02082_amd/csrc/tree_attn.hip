@@ -299,12 +299,14 @@ __device__ __forceinline__ bool visible(int j, int Lb, int k_end, int N, const u
   return m < (unsigned)N && ((anc[nt] >> m) & 1ull);
 }
 
-// One wave step: scores, softmax update, PV accumulation.
-template <int NT, bool TREE>
+// One wave step: scores, softmax update, PV accumulation.  With TILE_LB the
+// prefix length of tile nt is tile_lb[nt] instead of Lb (per-lane limits of
+// the block-masked kernel).
+template <int NT, bool TREE, bool TILE_LB = false>
 __device__ __forceinline__ void step(const Bf16Path::KV& f, const Bf16Path::QFrag (&qf)[NT],
                                      SoftmaxState (&sm)[NT], f32x4_t (&acc)[NT][8], int j0, int Lb,
                                      int k_end, int N, const uint64_t (&anc)[NT], float scale_log2,
-                                     int g) {
+                                     int g, const int* tile_lb = nullptr) {
   f32x4_t s[2][NT];
 #pragma unroll
   for (int kt = 0; kt < 2; ++kt)
@@ -331,16 +333,17 @@ __device__ __forceinline__ void step(const Bf16Path::KV& f, const Bf16Path::QFra
       vt[2 * w + 1][e] = __builtin_amdgcn_perm(b, a, 0x07060302u);  // high halves
     }
 
-  const bool need_mask = (j0 + 32 > min(Lb, k_end));
 #pragma unroll
   for (int nt = 0; nt < NT; ++nt) {
+    const int lb = TILE_LB ? tile_lb[nt] : Lb;
+    const bool need_mask = (j0 + 32 > min(lb, k_end));
     float x[8];
 #pragma unroll
     for (int kt = 0; kt < 2; ++kt)
 #pragma unroll
       for (int r = 0; r < 4; ++r) {
         float v = s[kt][nt][r];
-        if (need_mask && !visible<NT, TREE>(j0 + 16 * kt + 4 * g + r, Lb, k_end, N, anc, nt)) v = neg_inf();
+        if (need_mask && !visible<NT, TREE>(j0 + 16 * kt + 4 * g + r, lb, k_end, N, anc, nt)) v = neg_inf();
         x[4 * kt + r] = v;
       }
     float alpha;
@@ -865,38 +868,49 @@ constexpr int kSharedLds2 = 65536;
 // Block-masked cross attention of draft training (Sec. 4.1, "Block-wise
 // Attention Mask"): the query at position p sees the target's keys of the
 // earlier blocks, [0, block * floor(p / block)).  One workgroup per (head,
-// sequence, 64 query positions), one wave per 16-position tile, keys streamed
-// through the same LDS ring as the shared-step kernel, tiles with the most
-// keys first.  The mask is the cross-mode step's own: each lane (query) passes
-// its limit as the prefix length, which the step compares per key.
+// sequence, 64 * kNT query positions), kNT 16-position tiles per wave (each
+// K/V step read out of LDS once feeds every tile's products), keys streamed
+// through the same LDS ring as the shared-step kernel, workgroups with the
+// most keys first.  The mask is the cross-mode step's own: each lane (query)
+// passes its limit as its tile's prefix length, which the step compares per
+// key.
 // ---------------------------------------------------------------------------
-__global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(2)))
+template <int kNT>
+__global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(kNT <= 2 ? 2 : 1)))
 void block_attn_kernel(BlockAttnArgs args) {
   constexpr int kStages = kSharedLds4 / kStepBytes;
   constexpr int kStepInstr = kStepBytes / 1024 / kWaves;
+  constexpr int kBlockRows = 16 * kNT * kWaves;  // query positions per workgroup
   __shared__ __attribute__((aligned(1024))) char ring[kSharedLds4];
 
   const int h = blockIdx.x, b = blockIdx.y;
-  const int p0 = (gridDim.z - 1 - blockIdx.z) * 64;   // most keys first
+  const int p0 = (gridDim.z - 1 - blockIdx.z) * kBlockRows;  // most keys first
   const int tid = threadIdx.x, lane = tid & 63;
   const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
   const int c = lane & 15, g = lane >> 4;
   const int T = args.T, H = args.H, Lcap = args.L_cap, blk = args.block;
 
-  const int p_last = min(p0 + 63, T - 1);
+  const int p_last = min(p0 + kBlockRows - 1, T - 1);
   const int k_end = blk * (p_last / blk);            // the workgroup's largest limit
   const int steps = (k_end + 31) / 32;
-  const int p = p0 + 16 * wave + c;
-  const bool tile_live = p0 + 16 * wave < T;
-  const int my_limit = p < T ? blk * (p / blk) : 0;  // keys [0, my_limit) are visible
-  const uint64_t anc[1] = {0};
+  int p[kNT], my_limit[kNT];
+  bool live[kNT];
+  Bf16Path::QFrag qf[kNT];
+#pragma unroll
+  for (int nt = 0; nt < kNT; ++nt) {
+    const int row0 = p0 + 16 * (kNT * wave + nt);
+    p[nt] = row0 + c;
+    live[nt] = row0 < T;
+    my_limit[nt] = p[nt] < T ? blk * (p[nt] / blk) : 0;  // keys [0, limit) are visible
+    load_q<Bf16Path>(qf[nt], (const uint16_t*)args.q + (((size_t)b * T + min(p[nt], T - 1)) * H + h) * kD,
+                     p[nt] < T, g);
+  }
+  const bool any_live = live[0];  // tile 0 of a wave is live whenever tile 1 is
+  const uint64_t anc[kNT] = {};
 
   const size_t head_off = ((size_t)b * H + h) * (size_t)Lcap * kD;
   const char* kslab = (const char*)((const uint16_t*)args.k + head_off);
   const char* vslab = (const char*)((const uint16_t*)args.v + head_off);
-  Bf16Path::QFrag qf[1];
-  load_q<Bf16Path>(qf[0], (const uint16_t*)args.q + (((size_t)b * T + min(p, T - 1)) * H + h) * kD,
-                   p < T, g);
 
   const int dma_row = 4 * wave + (lane >> 4);
   const int dma_off = dma_row * 256 + 16 * ((lane & 15) ^ (dma_row & 15));
@@ -915,18 +929,21 @@ void block_attn_kernel(BlockAttnArgs args) {
 #pragma unroll
   for (int t = 0; t < kStages - 1; ++t) issue_step(t);
 
-  SoftmaxState sm[1];
-  sm[0].m = neg_inf();
-  sm[0].l = 0.f;
-  f32x4_t acc[1][8];
+  SoftmaxState sm[kNT];
+  f32x4_t acc[kNT][8];
 #pragma unroll
-  for (int t = 0; t < 8; ++t) acc[0][t] = f32x4_t{0.f, 0.f, 0.f, 0.f};
+  for (int nt = 0; nt < kNT; ++nt) {
+    sm[nt].m = neg_inf();
+    sm[nt].l = 0.f;
+#pragma unroll
+    for (int t = 0; t < 8; ++t) acc[nt][t] = f32x4_t{0.f, 0.f, 0.f, 0.f};
+  }
 
   for (int t = 0; t < steps; ++t) {
     ring_wait_and_meet<(kStages - 2) * kStepInstr>();
     issue_step(t + kStages - 1);
     const int j0 = 32 * t;
-    if (tile_live) {
+    if (any_live) {
       Bf16Path::KV f;
       read_step(f, ring + (t % kStages) * kStepBytes, c, g);
       if (j0 + 32 > k_end) {
@@ -934,19 +951,22 @@ void block_attn_kernel(BlockAttnArgs args) {
         for (int i = 0; i < 8; ++i)
           if (j0 + Bf16Path::key_slot(g, i) >= k_end) f.v[i] = u32x4_t{0, 0, 0, 0};
       }
-      step<1, false>(f, qf, sm, acc, j0, my_limit, k_end, 64, anc, args.scale_log2, g);
+      step<kNT, false, true>(f, qf, sm, acc, j0, 0, k_end, 64, anc, args.scale_log2, g, my_limit);
     }
   }
   asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
-  if (!tile_live) return;
-  const float L = sum_across_groups(sm[0].l);
-  const float inv = (L > 0.f) ? 1.f / L : 0.f;
 #pragma unroll
-  for (int r = 0; r < 4; ++r) {
-    float o[8];
+  for (int nt = 0; nt < kNT; ++nt) {
+    const float L = sum_across_groups(sm[nt].l);
+    const float inv = (L > 0.f) ? 1.f / L : 0.f;
 #pragma unroll
-    for (int t = 0; t < 8; ++t) o[t] = acc[0][t][r] * inv;
-    if (p < T) store_row8((uint16_t*)args.out + (((size_t)b * T + p) * H + h) * kD + 32 * g + 8 * r, o);
+    for (int r = 0; r < 4; ++r) {
+      float o[8];
+#pragma unroll
+      for (int t = 0; t < 8; ++t) o[t] = acc[nt][t][r] * inv;
+      if (p[nt] < T)
+        store_row8((uint16_t*)args.out + (((size_t)b * T + p[nt]) * H + h) * kD + 32 * g + 8 * r, o);
+    }
   }
 }
 
@@ -1030,8 +1050,14 @@ AttnPlan plan_tree_attn(int B, int N, int H, int L_cap, int max_splits) {
 }
 
 hipError_t launch_block_attn(const BlockAttnArgs& a, hipStream_t stream) {
-  const dim3 grid(a.H, a.B, (a.T + 63) / 64), block(kThreads);
-  hipLaunchKernelGGL(block_attn_kernel, grid, block, 0, stream, a);
+  // Two tiles per wave halve the LDS reads per query; take them while the
+  // grid still gives every CU two workgroups.
+  const long wgs2 = (long)a.H * a.B * ((a.T + 127) / 128);
+  if (wgs2 >= 2L * kNumCU) {
+    hipLaunchKernelGGL(block_attn_kernel<2>, dim3(a.H, a.B, (a.T + 127) / 128), dim3(kThreads), 0, stream, a);
+  } else {
+    hipLaunchKernelGGL(block_attn_kernel<1>, dim3(a.H, a.B, (a.T + 63) / 64), dim3(kThreads), 0, stream, a);
+  }
   return hipGetLastError();
 }
 

@@ -48,3 +48,16 @@ def test_training_shape_sampled():
     say("block_attn training shape", dict(T=T, positions=len(pos)))
     err, _ = _run(7, 2, T, 4, T, 5, positions=pos)
     assert err <= BF16_TOL, err
+
+
+def test_two_tile_launch_sampled():
+    """Enough (sequence, head, 128-position) groups for the two-tiles-per-wave
+    launch (B * H * ceil(T / 128) >= 512): T = 1100 leaves a ragged last group
+    whose second tiles lie partly past the end; blocks of 5."""
+    require_gpu()
+    T, H = 1100, 64
+    pos = sorted({0, 4, 5, 127, 128, 129, 255, 256, 600, 1023, 1024, 1050, 1087, 1088, 1095, 1099})
+    say("block_attn two-tile launch", dict(T=T, H=H, positions=len(pos)))
+    err, got = _run(11, 1, T, H, T, 5, positions=pos)
+    assert err <= BF16_TOL, err
+    assert np.all(got[:, :5] == 0)
