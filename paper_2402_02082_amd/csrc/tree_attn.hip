@@ -1,5 +1,6 @@
 // Split-K flash-decode attention of up to 64 query rows per (sequence, head)
-// against a KV cache, for gfx950.
+// against a KV cache, for gfx950; and the block-masked cross attention of
+// draft training, built from the same step.
 //
 // Computes hd = SoftMax(Q K^T * scale) V per head (arXiv 2402.02082, Sec. 4.1,
 // MultiHead / hd_j equations).  In tree mode a query row (tree node n) sees
@@ -9,31 +10,34 @@
 // the target cache, Sec. 4.1) every query row sees the prefix only.
 //
 // Work decomposition: one workgroup (4 waves) per (split, head, sequence).
-// A split owns a contiguous key range; its waves take interleaved 32-key
-// steps (16 for float32), so every K/V byte is read from HBM once and is
-// shared by all query rows of the sequence inside the MFMA tiles.  Up to 32
-// query rows (two 16-row tiles) each wave covers all of them; for 33..64 rows
-// the waves form two groups of two, one per pair of tiles, and each K/V step
-// is fetched by both groups (the second read hits L2).
+// A split owns a contiguous key range, so every K/V byte is read from HBM
+// once and is shared by all query rows of the sequence inside the MFMA tiles.
+//  * Register kernel (bf16 with 1..16 rows, float32 with up to 64): the waves
+//    take interleaved 32-key steps (16 for float32) with two steps of K/V in
+//    flight per wave in registers.  Float32 with 17..32 rows gives each wave
+//    both tiles; with 33..64 the waves form two groups of two, one per pair
+//    of tiles (the second group's read of a step hits L2).
+//  * Shared-step kernel (bf16 with 17..64 rows): each 32-key step goes from
+//    HBM straight into an LDS ring, where every wave owning one of the
+//    sequence's query tiles reads it.
 //
 // Per step and wave (bf16):
 //   S^T[key, query] = K Q^T   on v_mfma_f32_16x16x32_bf16, A = 16 key rows
-//                    (each lane loads 16 contiguous bytes of one key row),
+//                    (each lane holds 16 contiguous bytes of one key row),
 //                    B = the resident Q fragments;
 //   online softmax on S^T: the output layout puts one query per lane column,
 //                    so the running max/sum are per-lane scalars and only the
-//                    four 16-lane groups exchange their max (two shuffles);
+//                    four 16-lane groups exchange their max (two row swaps);
 //   O^T[d, query] += V^T P^T  on the same instruction, A = V^T built in
-//                    registers: each lane loads 16 contiguous bytes (8 head
+//                    registers: each lane holds 16 contiguous bytes (8 head
 //                    dims) of 8 key rows and transposes the 8x8 block with
 //                    byte permutes, B = P^T straight from the S^T registers.
 // Tree masking is only evaluated in steps that reach the tree rows, from a
 // 64-bit ancestor mask per query built by pointer doubling over the parents.
 //
-// Each wave keeps two or three steps of K/V loads in flight in registers.
-// The four waves merge their (max, sum, O) states through LDS.  With more
-// than one split per (sequence, head) each workgroup writes a partial state
-// and a second small kernel merges the partials in a fixed split order.
+// The waves merge their (max, sum, O) states through LDS.  With more than one
+// split per (sequence, head) each workgroup writes a partial state and a
+// second small kernel merges the partials in a fixed split order.
 #include <hip/hip_runtime.h>
 #include <stdint.h>
 
