@@ -243,6 +243,31 @@ int glide_rows_matmul(const void* a, const void* w_t, void* out, int M, int K, i
                       int out_dtype, hipStream_t stream);
 
 /*
+ * Packed weights for the projections (the same operation as
+ * glide_rows_matmul, Sec. 4.1).  From a row-major w_t every load of the
+ * projection fetches 64 bytes from each of 16 rows K * 2 bytes apart; the
+ * packed copy stores each (16-row tile, 32-wide K step) operand as one
+ * contiguous 1 KB block in the order the matrix cores take it: block
+ * (t, j) at byte (t * ceil(K / 32) + j) * 1024, its 16-byte unit l holding
+ * w_t[16t + l % 16][32j + 8 * (l / 16) .. + 7] (zeros past N or K).  Pack
+ * once (weights are static) and pass the copy to the *_packed calls; the
+ * results are bit-identical to the row-major calls.
+ *
+ * glide_rows_weights_packed_bytes -- bytes of the packed copy of a [N, K]
+ *   matrix, ceil(N / 16) * ceil(K / 32) * 1024; 0 for sizes
+ *   glide_rows_matmul rejects.  Host only.
+ * glide_pack_rows_weights -- writes the packed copy of w_t [N, K] bfloat16
+ *   (16-byte aligned) into w_packed (that many bytes, 16-byte aligned,
+ *   caller-allocated, not overlapping w_t).
+ * glide_rows_matmul_packed -- glide_rows_matmul with w_packed, the packed
+ *   copy of w_t for the same K and N.
+ */
+size_t glide_rows_weights_packed_bytes(int K, int N);
+int glide_pack_rows_weights(const void* w_t, void* w_packed, int K, int N, hipStream_t stream);
+int glide_rows_matmul_packed(const void* a, const void* w_packed, void* out, int M, int K, int N,
+                             int out_dtype, hipStream_t stream);
+
+/*
  * glide_cross_block -- MultiHead(Q^m, K^l, V^l) = Concat(hd_1..hd_h) W^O with
  * hd_j = SoftMax(Q^{m,j} (K^{l,j})^T / sqrt(d_k)) V^{l,j} and Q^{m,j} = H^m W_j
  * (Sec. 4.1): the draft's hidden rows projected into one query per target
@@ -262,6 +287,17 @@ int glide_cross_block(const void* hidden, const void* wq_t, const void* k_cache,
                       const void* v_cache, const int32_t* seq_lens, const void* wo_t, void* out,
                       int B, int Nq, int d_D, int H, int D, int L_cap, float scale,
                       void* workspace, size_t ws_bytes, hipStream_t stream);
+
+/*
+ * glide_cross_block_packed -- glide_cross_block with the two projections'
+ * weights in packed form: wq_packed the packed copy of wq_t (K = d_D,
+ * N = H*D) and wo_packed that of wo_t (K = H*D, N = d_D), as written by
+ * glide_pack_rows_weights.  Same workspace, results bit-identical.
+ */
+int glide_cross_block_packed(const void* hidden, const void* wq_packed, const void* k_cache,
+                             const void* v_cache, const int32_t* seq_lens, const void* wo_packed,
+                             void* out, int B, int Nq, int d_D, int H, int D, int L_cap, float scale,
+                             void* workspace, size_t ws_bytes, hipStream_t stream);
 
 /*
  * spec_sample_verify -- verification of a gamma-token draft chain with

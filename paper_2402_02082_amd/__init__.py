@@ -12,6 +12,8 @@ include/glide.h).  Functions carry the C names:
     glide_cross_block the GliDe cross-attention sub-layer (query projection,
                       cross attention, output projection)
     glide_rows_matmul its few-row projection
+    pack_rows_weights, glide_rows_matmul_packed, glide_cross_block_packed
+                      the same with weights packed once per 16-row operand tile
     glide_block_attn  the block-masked cross attention of draft training
     spec_sample_verify  chain verification with speculative sampling
     glide_expected_speedup  the expected-speedup model
@@ -23,7 +25,8 @@ from ._lib import (  # noqa: F401
     CAPE_MAX_K, GLIDE_BF16, GLIDE_EHIP, GLIDE_EINVAL, GLIDE_ERANGE, GLIDE_F32, GLIDE_OK,
     HEAD_DIM, MAX_NODES, MAX_SPLITS, GlideError, attn_workspace, cape_expand,
     cross_block_workspace, glide_argmax_rows, glide_block_attn, glide_cross_block,
-    glide_rows_matmul,
+    glide_cross_block_packed, glide_rows_matmul, glide_rows_matmul_packed, pack_rows_weights,
+    rows_weights_packed_bytes,
     glide_expected_speedup, glide_tree_attn, glide_verify_commit, load, spec_sample_verify,
     tree_verify,
 )

@@ -58,6 +58,14 @@ def load():
     lib.tree_verify.argtypes = [P, P, P, I, I, P, P, P, P]
     lib.glide_rows_matmul.restype = I
     lib.glide_rows_matmul.argtypes = [P, P, P, I, I, I, I, P]
+    lib.glide_rows_weights_packed_bytes.restype = Z
+    lib.glide_rows_weights_packed_bytes.argtypes = [I, I]
+    lib.glide_pack_rows_weights.restype = I
+    lib.glide_pack_rows_weights.argtypes = [P, P, I, I, P]
+    lib.glide_rows_matmul_packed.restype = I
+    lib.glide_rows_matmul_packed.argtypes = [P, P, P, I, I, I, I, P]
+    lib.glide_cross_block_packed.restype = I
+    lib.glide_cross_block_packed.argtypes = [P, P, P, P, P, P, P, I, I, I, I, I, I, F, P, Z, P]
     lib.glide_cross_block_workspace.restype = Z
     lib.glide_cross_block_workspace.argtypes = [I, I, I, I, I, I]
     lib.glide_cross_block.restype = I
@@ -78,7 +86,9 @@ def load():
 EXPORTED = ["glide_strerror", "glide_last_hip_error", "glide_tree_attn_workspace",
             "glide_tree_attn", "cape_expand_workspace", "cape_expand",
             "glide_argmax_rows", "tree_verify", "glide_verify_commit", "glide_rows_matmul",
-            "glide_cross_block_workspace", "glide_cross_block", "glide_block_attn",
+            "glide_rows_weights_packed_bytes", "glide_pack_rows_weights", "glide_rows_matmul_packed",
+            "glide_cross_block_workspace", "glide_cross_block", "glide_cross_block_packed",
+            "glide_block_attn",
             "spec_sample_verify",
             "glide_expected_speedup"]
 
@@ -277,6 +287,44 @@ def glide_rows_matmul(a, w_t, out, stream=None):
     return out
 
 
+def rows_weights_packed_bytes(K, N):
+    return load().glide_rows_weights_packed_bytes(K, N)
+
+
+def pack_rows_weights(w_t, out=None, stream=None):
+    """The packed copy of w_t [N, K] bfloat16 for the *_packed calls (a flat
+    bfloat16 tensor; see include/glide.h for the layout)."""
+    _dev(w_t, "w_t", torch.bfloat16)
+    _need(w_t.dim() == 2, "w_t must be [N, K]")
+    N, K = w_t.shape
+    need = rows_weights_packed_bytes(K, N)
+    _need(need > 0, "unsupported projection sizes")
+    if out is None:
+        out = torch.empty(need // 2, dtype=torch.bfloat16, device=w_t.device)
+    _dev(out, "out", torch.bfloat16)
+    _need(out.numel() * 2 >= need, "out is smaller than the packed copy")
+    status = load().glide_pack_rows_weights(_ptr(w_t), _ptr(out), K, N, _stream(stream, w_t.device))
+    _check("glide_pack_rows_weights", status)
+    return out
+
+
+def glide_rows_matmul_packed(a, w_packed, out, stream=None):
+    """glide_rows_matmul with the packed copy of w_t; N is out.shape[1]."""
+    _dev(a, "a", torch.bfloat16)
+    _dev(w_packed, "w_packed", torch.bfloat16)
+    _need(a.dim() == 2 and out.dim() == 2 and out.shape[0] == a.shape[0], "a must be [M, K], out [M, N]")
+    M, K = a.shape
+    N = out.shape[1]
+    _need(out.dtype in (torch.bfloat16, torch.float32), "out must be bfloat16 or float32")
+    _dev(out, "out")
+    _need(w_packed.numel() * 2 >= rows_weights_packed_bytes(K, N) > 0, "w_packed does not fit [N, K]")
+    status = load().glide_rows_matmul_packed(_ptr(a), _ptr(w_packed), _ptr(out), M, K, N,
+                                             GLIDE_BF16 if out.dtype == torch.bfloat16 else GLIDE_F32,
+                                             _stream(stream, a.device))
+    _check("glide_rows_matmul_packed", status)
+    return out
+
+
 def cross_block_workspace(B, Nq, d_D, H, L_cap, device):
     need = load().glide_cross_block_workspace(B, Nq, d_D, H, HEAD_DIM, L_cap)
     _need(need > 0, "unsupported cross-attention block sizes")
@@ -307,6 +355,34 @@ def glide_cross_block(hidden, wq_t, k_cache, v_cache, seq_lens, wo_t, out, scale
         _ptr(out), B, Nq, d_D, H, D, L_cap, float(scale), _ptr(workspace),
         workspace.numel() * workspace.element_size(), _stream(stream, hidden.device))
     _check("glide_cross_block", status)
+    return out
+
+
+def glide_cross_block_packed(hidden, wq_packed, k_cache, v_cache, seq_lens, wo_packed, out, scale=0.0,
+                             workspace=None, stream=None):
+    """glide_cross_block with both projections' weights packed
+    (pack_rows_weights of wq_t and of wo_t)."""
+    for name, t in (("hidden", hidden), ("wq_packed", wq_packed), ("k_cache", k_cache),
+                    ("v_cache", v_cache), ("wo_packed", wo_packed), ("out", out)):
+        _dev(t, name, torch.bfloat16)
+    _dev(seq_lens, "seq_lens", torch.int32)
+    B, Nq, d_D = hidden.shape
+    _need(k_cache.dim() == 4 and k_cache.shape[0] == B, "k_cache must be [B, H, L_cap, D]")
+    _need(v_cache.shape == k_cache.shape, "v_cache must match k_cache")
+    H, L_cap, D = k_cache.shape[1], k_cache.shape[2], k_cache.shape[3]
+    _need(wq_packed.numel() * 2 >= rows_weights_packed_bytes(d_D, H * D) > 0,
+          "wq_packed does not fit [H*D, d_D]")
+    _need(wo_packed.numel() * 2 >= rows_weights_packed_bytes(H * D, d_D) > 0,
+          "wo_packed does not fit [d_D, H*D]")
+    _need(tuple(out.shape) == (B, Nq, d_D), "out must be [B, Nq, d_D]")
+    _need(seq_lens.shape == (B,), "seq_lens must be [B]")
+    if workspace is None:
+        workspace = cross_block_workspace(B, Nq, d_D, H, L_cap, hidden.device)
+    status = load().glide_cross_block_packed(
+        _ptr(hidden), _ptr(wq_packed), _ptr(k_cache), _ptr(v_cache), _ptr(seq_lens), _ptr(wo_packed),
+        _ptr(out), B, Nq, d_D, H, D, L_cap, float(scale), _ptr(workspace),
+        workspace.numel() * workspace.element_size(), _stream(stream, hidden.device))
+    _check("glide_cross_block_packed", status)
     return out
 
 

@@ -248,12 +248,32 @@ int glide_verify_commit(const float* logits, int V, const int32_t* cand_tokens, 
   return hip_status(glide::launch_verify_commit(logits, V, a, stream));
 }
 
-int glide_rows_matmul(const void* a, const void* w_t, void* out, int M, int K, int N, int out_dtype,
-                      hipStream_t stream) {
-  if (!a || !w_t || !out || !aligned16(a) || !aligned16(w_t)) return GLIDE_EINVAL;
+static int rows_matmul_impl(const void* a, const void* w, void* out, int M, int K, int N,
+                            int out_dtype, bool packed, hipStream_t stream) {
+  if (!a || !w || !out || !aligned16(a) || !aligned16(w)) return GLIDE_EINVAL;
   if (!rows_matmul_sizes_ok(M, K, N)) return GLIDE_EINVAL;
   if (out_dtype != GLIDE_BF16 && out_dtype != GLIDE_F32) return GLIDE_EINVAL;
-  return hip_status(glide::launch_rows_matmul(a, w_t, out, M, K, N, out_dtype == GLIDE_BF16, stream));
+  return hip_status(glide::launch_rows_matmul(a, w, out, M, K, N, out_dtype == GLIDE_BF16, packed, stream));
+}
+
+int glide_rows_matmul(const void* a, const void* w_t, void* out, int M, int K, int N, int out_dtype,
+                      hipStream_t stream) {
+  return rows_matmul_impl(a, w_t, out, M, K, N, out_dtype, false, stream);
+}
+
+size_t glide_rows_weights_packed_bytes(int K, int N) {
+  return rows_matmul_sizes_ok(1, K, N) ? glide::packed_rows_weights_bytes(K, N) : 0;
+}
+
+int glide_pack_rows_weights(const void* w_t, void* w_packed, int K, int N, hipStream_t stream) {
+  if (!w_t || !w_packed || !aligned16(w_t) || !aligned16(w_packed)) return GLIDE_EINVAL;
+  if (!rows_matmul_sizes_ok(1, K, N)) return GLIDE_EINVAL;
+  return hip_status(glide::launch_pack_rows_weights(w_t, w_packed, K, N, stream));
+}
+
+int glide_rows_matmul_packed(const void* a, const void* w_packed, void* out, int M, int K, int N,
+                             int out_dtype, hipStream_t stream) {
+  return rows_matmul_impl(a, w_packed, out, M, K, N, out_dtype, true, stream);
 }
 
 size_t glide_cross_block_workspace(int B, int Nq, int d_D, int H, int D, int L_cap) {
@@ -261,10 +281,10 @@ size_t glide_cross_block_workspace(int B, int Nq, int d_D, int H, int D, int L_c
   return cross_block_plan(B, Nq, d_D, H, D, L_cap, &p) ? p.bytes : 0;
 }
 
-int glide_cross_block(const void* hidden, const void* wq_t, const void* k_cache, const void* v_cache,
-                      const int32_t* seq_lens, const void* wo_t, void* out, int B, int Nq, int d_D,
-                      int H, int D, int L_cap, float scale, void* workspace, size_t ws_bytes,
-                      hipStream_t stream) {
+static int cross_block_impl(const void* hidden, const void* wq_t, const void* k_cache,
+                            const void* v_cache, const int32_t* seq_lens, const void* wo_t, void* out,
+                            int B, int Nq, int d_D, int H, int D, int L_cap, float scale,
+                            void* workspace, size_t ws_bytes, bool packed, hipStream_t stream) {
   if (!hidden || !wq_t || !k_cache || !v_cache || !seq_lens || !wo_t || !out || !workspace)
     return GLIDE_EINVAL;
   if (!aligned16(hidden) || !aligned16(wq_t) || !aligned16(wo_t) || !aligned16(workspace))
@@ -283,13 +303,29 @@ int glide_cross_block(const void* hidden, const void* wq_t, const void* k_cache,
   void* q = ws + p.q_off;
   void* heads = ws + p.heads_off;
   const int M = B * Nq;
-  hipError_t e = glide::launch_rows_matmul(hidden, wq_t, q, M, d_D, H * D, true, stream);
+  hipError_t e = glide::launch_rows_matmul(hidden, wq_t, q, M, d_D, H * D, true, packed, stream);
   if (e != hipSuccess) return hip_status(e);
   const glide::AttnArgs a = attn_args(q, k_cache, v_cache, seq_lens, nullptr, heads, B, Nq, H, D,
                                       L_cap, scale, p.attn, ws + p.attn_off);
   e = glide::launch_tree_attn(a, true, stream);
   if (e != hipSuccess) return hip_status(e);
-  return hip_status(glide::launch_rows_matmul(heads, wo_t, out, M, H * D, d_D, true, stream));
+  return hip_status(glide::launch_rows_matmul(heads, wo_t, out, M, H * D, d_D, true, packed, stream));
+}
+
+int glide_cross_block(const void* hidden, const void* wq_t, const void* k_cache, const void* v_cache,
+                      const int32_t* seq_lens, const void* wo_t, void* out, int B, int Nq, int d_D,
+                      int H, int D, int L_cap, float scale, void* workspace, size_t ws_bytes,
+                      hipStream_t stream) {
+  return cross_block_impl(hidden, wq_t, k_cache, v_cache, seq_lens, wo_t, out, B, Nq, d_D, H, D, L_cap,
+                          scale, workspace, ws_bytes, false, stream);
+}
+
+int glide_cross_block_packed(const void* hidden, const void* wq_packed, const void* k_cache,
+                             const void* v_cache, const int32_t* seq_lens, const void* wo_packed,
+                             void* out, int B, int Nq, int d_D, int H, int D, int L_cap, float scale,
+                             void* workspace, size_t ws_bytes, hipStream_t stream) {
+  return cross_block_impl(hidden, wq_packed, k_cache, v_cache, seq_lens, wo_packed, out, B, Nq, d_D, H,
+                          D, L_cap, scale, workspace, ws_bytes, true, stream);
 }
 
 int glide_block_attn(const void* q, const void* k_cache, const void* v_cache, void* out, int B, int T,

@@ -22,8 +22,12 @@ hipError_t launch_argmax_rows(const float* logits, int rows, int V, int32_t* idx
 // kMaxMatmulRows rows per launch, more rows loop.
 constexpr int kMaxMatmulRows = 64;
 constexpr int kMaxMatmulK = 1 << 20;
-hipError_t launch_rows_matmul(const void* a, const void* w_t, void* out, int M, int K, int N,
-                              bool out_bf16, hipStream_t stream);
+hipError_t launch_rows_matmul(const void* a, const void* w, void* out, int M, int K, int N,
+                              bool out_bf16, bool packed, hipStream_t stream);
+// Bytes of the packed copy of a [N, K] weight matrix: one 1 KB operand block
+// per (16-row tile, 32-wide K step).
+size_t packed_rows_weights_bytes(int K, int N);
+hipError_t launch_pack_rows_weights(const void* w_t, void* packed, int K, int N, hipStream_t stream);
 
 hipError_t launch_spec_sample(const int32_t* draft_tokens, const float* p_draft, const float* p_target,
                               const float* uniforms, int B, int gamma, int V, int32_t* accept_len,

@@ -13,6 +13,14 @@
 // same operand shapes as the attention kernel's K * Q^T.  Loads go through
 // range-checked buffer descriptors (weight rows past N and activation rows
 // past M read as zeros), eight steps in flight per wave in registers.
+//
+// An operand tile spans 16 weight rows, so from a row-major w_t each load
+// instruction fetches 64 bytes from each of 16 rows K * 2 bytes apart.  The
+// packed layout (pack_rows_weights_kernel) stores every (16-row tile,
+// 32-wide K step) operand as one 1 KB block in lane order -- lane l holds
+// row l % 16, k 8 * (l / 16) .. + 7 -- so the same registers arrive from one
+// contiguous 1 KB read.  Packing is a one-time transformation of static
+// weights; both layouts give bit-identical results.
 #include <hip/hip_runtime.h>
 #include <stdint.h>
 
@@ -42,14 +50,16 @@ struct Step {
   u32x4_t a[MT];
 };
 
-template <int MT>
+template <int MT, bool PACKED>
 __device__ __forceinline__ void load_step(Step<MT>& s, __amdgpu_buffer_rsrc_t rw, __amdgpu_buffer_rsrc_t ra,
-                                          int w_off, int a_off, int a_tile_stride, int kk, int K) {
+                                          int w_off, int a_off, int a_tile_stride, int step, int g, int K) {
   // kk: this lane's first k of the step; K % 8 == 0, so a lane's 8 values are
   // all inside the row or all past it.  Past it, the offset moves beyond
   // every descriptor's range, so the load returns zeros (no branch).
+  const int kk = 32 * step + 8 * g;
   const int kb = kk < K ? kk * 2 : kOutOfRange;
-  s.w = load16<kStream>(rw, w_off + kb);
+  // packed: step `step` of the tile is the 1 KB block at step * 1024
+  s.w = load16<kStream>(rw, PACKED ? (kk < K ? step * 1024 + w_off : kOutOfRange) : w_off + kb);
 #pragma unroll
   for (int t = 0; t < MT; ++t) s.a[t] = load16<0>(ra, a_off + t * a_tile_stride + kb);
 }
@@ -67,7 +77,7 @@ __device__ __forceinline__ void store_out(uint16_t* p, float v) {
   *p = __builtin_bit_cast(uint16_t, (__bf16)v);
 }
 
-template <int MT, class OutT>
+template <int MT, class OutT, bool PACKED>
 __global__ __launch_bounds__(64 * kWaves) void rows_matmul_kernel(const uint16_t* __restrict__ a,
                                                                   const uint16_t* __restrict__ w_t,
                                                                   OutT* __restrict__ out, int M,
@@ -78,11 +88,17 @@ __global__ __launch_bounds__(64 * kWaves) void rows_matmul_kernel(const uint16_t
   // weight rows n0 .. n0 + 15 and activation rows 0 .. M - 1; rows past the
   // ends read as zeros
   const int w_rows = min(16, N - n0);
-  const __amdgpu_buffer_rsrc_t rw = __builtin_amdgcn_make_buffer_rsrc(
-      const_cast<uint16_t*>(w_t) + (size_t)n0 * K, (short)0, w_rows * K * 2, kDesc3);
+  const int k_steps = (K + 31) / 32;
+  // row-major: rows n0 .. n0 + w_rows - 1; packed: the tile's k_steps blocks
+  // (rows past N are zeros in the packed copy)
+  const __amdgpu_buffer_rsrc_t rw = PACKED
+      ? __builtin_amdgcn_make_buffer_rsrc(const_cast<uint16_t*>(w_t) + (size_t)blockIdx.x * k_steps * 512,
+                                          (short)0, k_steps * 1024, kDesc3)
+      : __builtin_amdgcn_make_buffer_rsrc(const_cast<uint16_t*>(w_t) + (size_t)n0 * K, (short)0,
+                                          w_rows * K * 2, kDesc3);
   const __amdgpu_buffer_rsrc_t ra = __builtin_amdgcn_make_buffer_rsrc(const_cast<uint16_t*>(a), (short)0,
                                                                       M * K * 2, kDesc3);
-  const int w_off = c * K * 2;       // A operand: weight row n0 + c
+  const int w_off = PACKED ? 16 * lane : c * K * 2;  // A operand: weight row n0 + c
   const int a_off = c * K * 2;       // B operand: activation row 16 t + c
   const int a_tile_stride = 16 * K * 2;
 
@@ -97,13 +113,13 @@ __global__ __launch_bounds__(64 * kWaves) void rows_matmul_kernel(const uint16_t
   int s = wave;  // this wave's steps: wave, wave + 4, ...
 #pragma unroll
   for (int u = 0; u < kBufs; ++u)
-    load_step<MT>(buf[u], rw, ra, w_off, a_off, a_tile_stride, 32 * (s + u * kWaves) + 8 * g, K);
+    load_step<MT, PACKED>(buf[u], rw, ra, w_off, a_off, a_tile_stride, s + u * kWaves, g, K);
   __builtin_amdgcn_sched_barrier(0);
   for (int it = 0; it + 1 < iters; ++it) {
 #pragma unroll
     for (int u = 0; u < kBufs; ++u) {
       mma_step<MT>(buf[u], acc);
-      load_step<MT>(buf[u], rw, ra, w_off, a_off, a_tile_stride, 32 * (s + kBufs * kWaves) + 8 * g, K);
+      load_step<MT, PACKED>(buf[u], rw, ra, w_off, a_off, a_tile_stride, s + kBufs * kWaves, g, K);
       s += kWaves;
     }
   }
@@ -135,33 +151,72 @@ __global__ __launch_bounds__(64 * kWaves) void rows_matmul_kernel(const uint16_t
   }
 }
 
-template <class OutT>
+template <class OutT, bool PACKED>
 hipError_t launch_rows(const uint16_t* a, const uint16_t* w_t, OutT* out, int M, int K, int N,
                        hipStream_t stream) {
   const dim3 grid((N + 15) / 16), block(64 * kWaves);
   const int mt = (M + 15) / 16;
   if (mt == 1)
-    hipLaunchKernelGGL((rows_matmul_kernel<1, OutT>), grid, block, 0, stream, a, w_t, out, M, K, N);
+    hipLaunchKernelGGL((rows_matmul_kernel<1, OutT, PACKED>), grid, block, 0, stream, a, w_t, out, M, K, N);
   else if (mt == 2)
-    hipLaunchKernelGGL((rows_matmul_kernel<2, OutT>), grid, block, 0, stream, a, w_t, out, M, K, N);
+    hipLaunchKernelGGL((rows_matmul_kernel<2, OutT, PACKED>), grid, block, 0, stream, a, w_t, out, M, K, N);
   else if (mt == 3)
-    hipLaunchKernelGGL((rows_matmul_kernel<3, OutT>), grid, block, 0, stream, a, w_t, out, M, K, N);
+    hipLaunchKernelGGL((rows_matmul_kernel<3, OutT, PACKED>), grid, block, 0, stream, a, w_t, out, M, K, N);
   else
-    hipLaunchKernelGGL((rows_matmul_kernel<4, OutT>), grid, block, 0, stream, a, w_t, out, M, K, N);
+    hipLaunchKernelGGL((rows_matmul_kernel<4, OutT, PACKED>), grid, block, 0, stream, a, w_t, out, M, K, N);
   return hipGetLastError();
+}
+
+// One thread per 16-byte unit of the packed copy: unit u of tile t, step j
+// is lane u % 64 of that step's operand -- row 16t + (u % 16), k
+// 32j + 8 * (u % 64 / 16) .. + 7 of w_t, or zeros past N or K.
+__global__ __launch_bounds__(256) void pack_rows_weights_kernel(const uint16_t* __restrict__ w_t,
+                                                                uint16_t* __restrict__ packed, int K,
+                                                                int N, long units) {
+  const long u = (long)blockIdx.x * 256 + threadIdx.x;
+  if (u >= units) return;
+  const int k_steps = (K + 31) / 32;
+  const int l = (int)(u % 64);
+  const long blk = u / 64;  // tile * k_steps + step
+  const int step = (int)(blk % k_steps);
+  const long tile = blk / k_steps;
+  const long row = tile * 16 + (l & 15);
+  const int k0 = 32 * step + 8 * (l >> 4);
+  u32x4_t v = {0, 0, 0, 0};
+  if (row < N && k0 < K) v = *(const u32x4_t*)(w_t + row * K + k0);
+  *(u32x4_t*)(packed + u * 8) = v;
 }
 
 }  // namespace
 
-hipError_t launch_rows_matmul(const void* a, const void* w_t, void* out, int M, int K, int N,
-                              bool out_bf16, hipStream_t stream) {
+size_t packed_rows_weights_bytes(int K, int N) {
+  return (size_t)((N + 15) / 16) * ((K + 31) / 32) * 1024;
+}
+
+hipError_t launch_pack_rows_weights(const void* w_t, void* packed, int K, int N, hipStream_t stream) {
+  const long units = (long)(packed_rows_weights_bytes(K, N) / 16);
+  hipLaunchKernelGGL(pack_rows_weights_kernel, dim3((unsigned)((units + 255) / 256)), dim3(256), 0, stream,
+                     (const uint16_t*)w_t, (uint16_t*)packed, K, N, units);
+  return hipGetLastError();
+}
+
+hipError_t launch_rows_matmul(const void* a, const void* w, void* out, int M, int K, int N,
+                              bool out_bf16, bool packed, hipStream_t stream) {
   // at most 64 activation rows per launch; more rows take further launches
   for (int m0 = 0; m0 < M; m0 += kMaxMatmulRows) {
     const int rows = min(kMaxMatmulRows, M - m0);
     const uint16_t* ap = (const uint16_t*)a + (size_t)m0 * K;
-    hipError_t e = out_bf16
-                       ? launch_rows(ap, (const uint16_t*)w_t, (uint16_t*)out + (size_t)m0 * N, rows, K, N, stream)
-                       : launch_rows(ap, (const uint16_t*)w_t, (float*)out + (size_t)m0 * N, rows, K, N, stream);
+    const uint16_t* wp = (const uint16_t*)w;
+    hipError_t e;
+    if (out_bf16) {
+      uint16_t* op = (uint16_t*)out + (size_t)m0 * N;
+      e = packed ? launch_rows<uint16_t, true>(ap, wp, op, rows, K, N, stream)
+                 : launch_rows<uint16_t, false>(ap, wp, op, rows, K, N, stream);
+    } else {
+      float* op = (float*)out + (size_t)m0 * N;
+      e = packed ? launch_rows<float, true>(ap, wp, op, rows, K, N, stream)
+                 : launch_rows<float, false>(ap, wp, op, rows, K, N, stream);
+    }
     if (e != hipSuccess) return e;
   }
   return hipSuccess;

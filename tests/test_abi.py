@@ -163,6 +163,34 @@ def test_rows_matmul_rejects(lib, args):
     assert lib.glide_rows_matmul(*args, None) == glide.GLIDE_EINVAL
 
 
+def test_rows_weights_packed_bytes(lib):
+    # one 1 KB block per (16-row tile, 32-wide K step)
+    assert lib.glide_rows_weights_packed_bytes(4096, 4096) == 256 * 128 * 1024
+    assert lib.glide_rows_weights_packed_bytes(40, 17) == 2 * 2 * 1024
+    assert lib.glide_rows_weights_packed_bytes(8, 1) == 1024
+    for K, N in ((12, 16), (0, 16), (4096, 0), ((1 << 20) + 8, 16)):
+        assert lib.glide_rows_weights_packed_bytes(K, N) == 0
+
+
+@pytest.mark.parametrize("args", [
+    (None, FAKE, 4096, 4096), (FAKE, None, 4096, 4096), (ctypes.c_void_p(0x1008), FAKE, 4096, 4096),
+    (FAKE, ctypes.c_void_p(0x1004), 4096, 4096), (FAKE, FAKE, 12, 4096), (FAKE, FAKE, 0, 4096),
+    (FAKE, FAKE, 4096, 0),
+])
+def test_pack_rows_weights_rejects(lib, args):
+    assert lib.glide_pack_rows_weights(*args, None) == glide.GLIDE_EINVAL
+
+
+@pytest.mark.parametrize("args", [
+    (None, FAKE, FAKE, 5, 4096, 4096, 0), (FAKE, None, FAKE, 5, 4096, 4096, 0),
+    (FAKE, FAKE, None, 5, 4096, 4096, 0), (FAKE, ctypes.c_void_p(0x1008), FAKE, 5, 4096, 4096, 0),
+    (FAKE, FAKE, FAKE, 0, 4096, 4096, 0), (FAKE, FAKE, FAKE, 5, 12, 4096, 0),
+    (FAKE, FAKE, FAKE, 5, 4096, 0, 0), (FAKE, FAKE, FAKE, 5, 4096, 4096, 2),
+])
+def test_rows_matmul_packed_rejects(lib, args):
+    assert lib.glide_rows_matmul_packed(*args, None) == glide.GLIDE_EINVAL
+
+
 def test_cross_block_workspace(lib):
     rows = 1 * 5 * 32 * 128 * 2                      # bf16 [B, Nq, H, D], 256-aligned already
     attn = lib.glide_tree_attn_workspace(1, 5, 32, 128, 2064, 0)
@@ -189,6 +217,12 @@ def _xblock(lib, **kw):
 ])
 def test_cross_block_rejects(lib, bad):
     assert _xblock(lib, **bad) == glide.GLIDE_EINVAL
+    a = dict(h=FAKE, wq=FAKE, k=FAKE, v=FAKE, lens=FAKE, wo=FAKE, out=FAKE, B=1, Nq=5, dD=4096,
+             H=32, D=128, L_cap=2064, scale=0.0, ws=FAKE, ws_bytes=1 << 30)
+    a.update(bad)
+    assert lib.glide_cross_block_packed(a["h"], a["wq"], a["k"], a["v"], a["lens"], a["wo"], a["out"],
+                                        a["B"], a["Nq"], a["dD"], a["H"], a["D"], a["L_cap"],
+                                        a["scale"], a["ws"], a["ws_bytes"], None) == glide.GLIDE_EINVAL
 
 
 @pytest.mark.parametrize("args", [

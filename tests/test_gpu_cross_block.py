@@ -103,3 +103,69 @@ def test_cross_block_workload(cfg):
                               to64(v[b:b + 1, :, :L]), [L], to64(wo_t), store=torch.bfloat16)
         excess = bf16_ok(to64(out[b:b + 1]), want)
         assert excess <= 0, (b, excess)
+
+
+@pytest.mark.parametrize("M,K,N", [(1, 8, 1), (5, 4096, 4096), (17, 512, 100), (64, 1024, 333),
+                                   (130, 256, 48), (3, 4104, 16), (5, 40, 4097)])
+@pytest.mark.parametrize("out_dtype", [torch.float32, torch.bfloat16])
+def test_rows_matmul_packed(M, K, N, out_dtype):
+    """Packed weights: the same registers reach the matrix cores, so the
+    result is bit-identical to the row-major call, and within the bound of the
+    oracle; ragged N (partial last tile) and K (partial last step) included."""
+    require_gpu()
+    say("rows_matmul packed", dict(M=M, K=K, N=N, out=str(out_dtype)))
+    a = _bf16((M, K), 11 + M).cuda()
+    w_t = _bf16((N, K), 12 + N, 1.0 / np.sqrt(K)).cuda()
+    packed = glide.pack_rows_weights(w_t)
+    assert packed.numel() * 2 == ((N + 15) // 16) * ((K + 31) // 32) * 1024
+    got = torch.full((M, N), float("nan"), dtype=out_dtype, device="cuda")
+    ref = torch.full((M, N), float("nan"), dtype=out_dtype, device="cuda")
+    glide.glide_rows_matmul_packed(a, packed, got)
+    glide.glide_rows_matmul(a, w_t, ref)
+    torch.cuda.synchronize()
+    assert torch.equal(got.view(torch.int16 if out_dtype == torch.bfloat16 else torch.int32),
+                       ref.view(torch.int16 if out_dtype == torch.bfloat16 else torch.int32))
+    want = OX.rows_matmul(to64(a), to64(w_t))
+    if out_dtype == torch.float32:
+        err = float(np.abs(to64(got) - want).max())
+        assert err <= F32_OUT_TOL, err
+    else:
+        excess = bf16_ok(to64(got), want)
+        assert excess <= 0, excess
+
+
+def test_pack_layout():
+    """Unit l of block (t, j) holds w_t[16t + l % 16][32j + 8 (l / 16) .. + 7],
+    zeros past N and K (K = 40, N = 17: both edges)."""
+    require_gpu()
+    K, N = 40, 17
+    w_t = (torch.arange(N * K, dtype=torch.float32).reshape(N, K) % 251).to(torch.bfloat16)
+    packed = glide.pack_rows_weights(w_t.cuda()).cpu().view(-1, 8)   # 16-byte units
+    ksteps = (K + 31) // 32
+    for u in range(packed.shape[0]):
+        blk, l = divmod(u, 64)
+        t, j = divmod(blk, ksteps)
+        row, k0 = 16 * t + l % 16, 32 * j + 8 * (l // 16)
+        want = w_t[row, k0:k0 + 8] if row < N and k0 < K else torch.zeros(8, dtype=torch.bfloat16)
+        assert torch.equal(packed[u].view(torch.int16), want.view(torch.int16)), u
+
+
+@pytest.mark.parametrize("B,Nq,H,d_D,L_cap,lens", [
+    (1, 5, 2, 256, 300, [300]),
+    (3, 7, 4, 520, 700, [0, 1, 699]),
+])
+def test_cross_block_packed(B, Nq, H, d_D, L_cap, lens):
+    require_gpu()
+    say("cross_block packed", dict(B=B, Nq=Nq, H=H, d_D=d_D, L_cap=L_cap, lens=lens))
+    hidden, wq_t, k, v, sl, wo_t = _block_case(17 + B, B, Nq, H, d_D, L_cap, lens)
+    got = torch.full_like(hidden, float("nan"))
+    ref = torch.full_like(hidden, float("nan"))
+    glide.glide_cross_block_packed(hidden, glide.pack_rows_weights(wq_t), k, v, sl,
+                                   glide.pack_rows_weights(wo_t), got)
+    glide.glide_cross_block(hidden, wq_t, k, v, sl, wo_t, ref)
+    torch.cuda.synchronize()
+    assert torch.equal(got.view(torch.int16), ref.view(torch.int16))
+    want = OX.cross_block(to64(hidden), to64(wq_t), to64(k), to64(v), lens, to64(wo_t),
+                          store=torch.bfloat16)
+    excess = bf16_ok(to64(got), want)
+    assert excess <= 0, excess
