@@ -64,6 +64,69 @@ __device__ uint64_t block_exclusive_scan(uint64_t x, uint64_t* total) {
   return before + incl - x;
 }
 
+// Up to kHeld tokens per thread (V <= 4 * kThreads * 8 = 32768): the pass
+// that sums a thread's chunk also parks the chosen row's per-token values in
+// LDS (element-major, so a wave's stores are conflict-free), and the owner of
+// the drawn chunk searches them there instead of reading the rows again.
+constexpr int kHeld = 32;
+
+__device__ uint64_t held_weight(float* held, const float* pt, const float* pd, int v0, int v1, int mode,
+                                bool vec) {
+  const int tid = threadIdx.x;
+  uint64_t sum = 0;
+  if (vec) {
+#pragma unroll 2
+    for (int i = 0; i < kHeld; i += 4) {
+      const int v = v0 + i;
+      float4 a = make_float4(0.f, 0.f, 0.f, 0.f), d = a;
+      if (v < v1) {
+        a = *(const float4*)(pt + v);
+        if (mode == 0) d = *(const float4*)(pd + v);
+      }
+      const float av[4] = {a.x, a.y, a.z, a.w}, dv[4] = {d.x, d.y, d.z, d.w};
+#pragma unroll
+      for (int e = 0; e < 4; ++e) {
+        float p = av[e];
+        if (mode == 0) {
+          const float r = av[e] - dv[e];
+          p = r > 0.f ? r : 0.f;
+        }
+        held[(i + e) * kThreads + tid] = p;
+        sum += fixed_weight(p);
+      }
+    }
+  } else {
+    for (int i = 0; i < kHeld; ++i) {
+      const int v = v0 + i;
+      float p = 0.f;
+      if (v < v1) {
+        p = pt[v];
+        if (mode == 0) {
+          const float r = p - pd[v];
+          p = r > 0.f ? r : 0.f;
+        }
+      }
+      held[i * kThreads + tid] = p;
+      sum += fixed_weight(p);
+    }
+  }
+  return sum;
+}
+
+__device__ int held_find(const float* held, int v0, int v1, uint64_t run, uint64_t t) {
+  const int tid = threadIdx.x;
+  int found = v1 - 1;
+  bool done = false;
+  for (int i = 0; i < kHeld && v0 + i < v1; ++i) {
+    run += fixed_weight(held[i * kThreads + tid]);
+    if (!done && run > t) {
+      found = v0 + i;
+      done = true;
+    }
+  }
+  return found;
+}
+
 // Sum of the weights of tokens [v0, v1).
 __device__ uint64_t chunk_weight(const float* pt, const float* pd, int v0, int v1, int mode, bool vec) {
   uint64_t sum = 0;
@@ -125,6 +188,7 @@ __device__ int chunk_find(const float* pt, const float* pd, int v0, int v1, int 
   return found;
 }
 
+template <bool KEEP>
 __global__ __launch_bounds__(kThreads) void spec_sample_kernel(const int32_t* __restrict__ draft_tokens,
                                                                const float* __restrict__ p_draft,
                                                                const float* __restrict__ p_target,
@@ -160,9 +224,11 @@ __global__ __launch_bounds__(kThreads) void spec_sample_kernel(const int32_t* __
   const int v0 = min(V, tid * chunk), v1 = min(V, v0 + chunk);
   const bool vec = (V & 3) == 0 && ((((uintptr_t)p_target) | ((uintptr_t)p_draft)) & 15) == 0;
   int mode = j < gamma ? 0 : 1;
+  // KEEP (chunk <= kHeld): the chunk fits the LDS copy, so the rows are read once
+  __shared__ float held[KEEP ? kHeld * kThreads : 1];
   uint64_t total = 0, mine = 0, before = 0;
   for (int pass = 0; pass < 2; ++pass) {
-    mine = chunk_weight(pt, pd, v0, v1, mode, vec);
+    mine = KEEP ? held_weight(held, pt, pd, v0, v1, mode, vec) : chunk_weight(pt, pd, v0, v1, mode, vec);
     before = block_exclusive_scan(mine, &total);
     if (total > 0 || mode == 1) break;
     mode = 1;  // a residual of zero weight: draw from the target row itself
@@ -178,7 +244,8 @@ __global__ __launch_bounds__(kThreads) void spec_sample_kernel(const int32_t* __
   if (t >= total) t = total - 1;
   if (before <= t && t < before + mine) {
     accept_len[b] = j;
-    next_token[b] = chunk_find(pt, pd, v0, v1, mode, vec, before, t);
+    // the owner reads back its own LDS entries (no barrier needed)
+    next_token[b] = KEEP ? held_find(held, v0, v1, before, t) : chunk_find(pt, pd, v0, v1, mode, vec, before, t);
   }
 }
 
@@ -187,8 +254,13 @@ __global__ __launch_bounds__(kThreads) void spec_sample_kernel(const int32_t* __
 hipError_t launch_spec_sample(const int32_t* draft_tokens, const float* p_draft, const float* p_target,
                               const float* uniforms, int B, int gamma, int V, int32_t* accept_len,
                               int32_t* next_token, hipStream_t stream) {
-  hipLaunchKernelGGL(spec_sample_kernel, dim3(B), dim3(kThreads), 0, stream, draft_tokens, p_draft,
-                     p_target, uniforms, gamma, V, accept_len, next_token);
+  const int chunk = ((V + 4 * kThreads - 1) / (4 * kThreads)) * 4;
+  if (chunk <= kHeld)
+    hipLaunchKernelGGL(spec_sample_kernel<true>, dim3(B), dim3(kThreads), 0, stream, draft_tokens, p_draft,
+                       p_target, uniforms, gamma, V, accept_len, next_token);
+  else
+    hipLaunchKernelGGL(spec_sample_kernel<false>, dim3(B), dim3(kThreads), 0, stream, draft_tokens, p_draft,
+                       p_target, uniforms, gamma, V, accept_len, next_token);
   return hipGetLastError();
 }
 

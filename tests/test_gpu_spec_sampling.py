@@ -44,7 +44,10 @@ def make_case(seed, B, gamma, V, mode):
 
 
 @pytest.mark.parametrize("B,gamma,V", [(1, 5, 32000), (16, 5, 32000), (4, 1, 7), (3, 8, 1000),
-                                       (2, 64, 300), (5, 5, 1), (8, 3, 1025)])
+                                       (2, 64, 300), (5, 5, 1), (8, 3, 1025),
+                                       # the last vocabulary whose chunks are kept in LDS, the
+                                       # first that reads its rows twice, and an odd one past it
+                                       (2, 5, 32768), (2, 5, 32769), (2, 3, 65537)])
 @pytest.mark.parametrize("mode", ["mixed", "same", "zero", "scaled"])
 def test_parity(B, gamma, V, mode):
     require_gpu()
