@@ -128,3 +128,38 @@ def test_graph_replays_match_eager():
                 else torch.equal(a, b)
             assert same, (rep, k)
     del graph
+
+
+def test_two_streams_own_workspaces():
+    """Split-plan attention and the cross block issued on two streams at once:
+    the binding keeps one workspace per (device, stream), so the calls do not
+    share partial states and each matches its single-stream result."""
+    require_gpu()
+    say("two streams")
+    st = _inputs()
+    other = _inputs()
+    other["q"] = other["q"].flip(0).contiguous()        # different queries on the second stream
+    other["hidden"] = (other["hidden"] * 0.5).contiguous()
+    work = lambda d: (glide.glide_tree_attn(d["q"], d["kc"], d["vc"], d["lens"], d["par32"][:, :16].contiguous(),  # noqa: E731
+                                             d["out"]),
+                      glide.glide_cross_block_packed(d["hidden"], d["wq_p"], d["kc"], d["vc"], d["lens"],
+                                                     d["wo_p"], d["xb_out"]))
+    work(st)
+    work(other)
+    torch.cuda.synchronize()
+    want = (st["out"].clone(), st["xb_out"].clone(), other["out"].clone(), other["xb_out"].clone())
+    for d in (st, other):
+        d["out"].fill_(float("nan"))
+        d["xb_out"].fill_(float("nan"))
+    s1, s2 = torch.cuda.Stream(), torch.cuda.Stream()
+    s1.wait_stream(torch.cuda.current_stream())
+    s2.wait_stream(torch.cuda.current_stream())
+    for _ in range(3):
+        with torch.cuda.stream(s1):
+            work(st)
+        with torch.cuda.stream(s2):
+            work(other)
+    torch.cuda.synchronize()
+    got = (st["out"], st["xb_out"], other["out"], other["xb_out"])
+    for a, b in zip(got, want):
+        assert torch.equal(a.view(torch.int16), b.view(torch.int16))
