@@ -303,14 +303,26 @@ __device__ __forceinline__ bool visible(int j, int Lb, int k_end, int N, const u
   return m < (unsigned)N && ((anc[nt] >> m) & 1ull);
 }
 
-// One wave step: scores, softmax update, PV accumulation.  With TILE_LB the
-// prefix length of tile nt is tile_lb[nt] instead of Lb (per-lane limits of
-// the block-masked kernel).
-template <int NT, bool TREE, bool TILE_LB = false>
+// V^T operands of a step: tile t holds head dim 8*c + t of the 8 keys of
+// this lane's k-slots, i.e. element t of each loaded 8-dim chunk, two keys
+// per dword (one byte permute per dword).
+__device__ __forceinline__ void transpose_v(const u32x4_t (&v)[8], u32x4_t (&vt)[8]) {
+#pragma unroll
+  for (int w = 0; w < 4; ++w)
+#pragma unroll
+    for (int e = 0; e < 4; ++e) {
+      const uint32_t a = v[2 * e][w], b = v[2 * e + 1][w];
+      vt[2 * w][e] = __builtin_amdgcn_perm(b, a, 0x05040100u);      // low halves
+      vt[2 * w + 1][e] = __builtin_amdgcn_perm(b, a, 0x07060302u);  // high halves
+    }
+}
+
+// One wave step: scores, softmax update, PV accumulation.
+template <int NT, bool TREE>
 __device__ __forceinline__ void step(const Bf16Path::KV& f, const Bf16Path::QFrag (&qf)[NT],
                                      SoftmaxState (&sm)[NT], f32x4_t (&acc)[NT][8], int j0, int Lb,
                                      int k_end, int N, const uint64_t (&anc)[NT], float scale_log2,
-                                     int g, const int* tile_lb = nullptr) {
+                                     int g) {
   f32x4_t s[2][NT];
 #pragma unroll
   for (int kt = 0; kt < 2; ++kt)
@@ -324,30 +336,19 @@ __device__ __forceinline__ void step(const Bf16Path::KV& f, const Bf16Path::QFra
       s[kt][nt] = a;
     }
 
-  // V^T operands: tile t holds head dim 8*c + t of the 8 keys of this lane's
-  // k-slots, i.e. element t of each loaded 8-dim chunk, two keys per dword
-  // (one byte permute per dword).
   u32x4_t vt[8];
-#pragma unroll
-  for (int w = 0; w < 4; ++w)
-#pragma unroll
-    for (int e = 0; e < 4; ++e) {
-      const uint32_t a = f.v[2 * e][w], b = f.v[2 * e + 1][w];
-      vt[2 * w][e] = __builtin_amdgcn_perm(b, a, 0x05040100u);      // low halves
-      vt[2 * w + 1][e] = __builtin_amdgcn_perm(b, a, 0x07060302u);  // high halves
-    }
+  transpose_v(f.v, vt);
 
 #pragma unroll
   for (int nt = 0; nt < NT; ++nt) {
-    const int lb = TILE_LB ? tile_lb[nt] : Lb;
-    const bool need_mask = (j0 + 32 > min(lb, k_end));
+    const bool need_mask = (j0 + 32 > min(Lb, k_end));
     float x[8];
 #pragma unroll
     for (int kt = 0; kt < 2; ++kt)
 #pragma unroll
       for (int r = 0; r < 4; ++r) {
         float v = s[kt][nt][r];
-        if (need_mask && !visible<NT, TREE>(j0 + 16 * kt + 4 * g + r, lb, k_end, N, anc, nt)) v = neg_inf();
+        if (need_mask && !visible<NT, TREE>(j0 + 16 * kt + 4 * g + r, Lb, k_end, N, anc, nt)) v = neg_inf();
         x[4 * kt + r] = v;
       }
     float alpha;
@@ -868,6 +869,107 @@ constexpr int kSharedLds4 = 65536;
 constexpr int kSharedLds2 = 65536;
 
 
+// One 32-key step of the block-masked kernel for the wave's NT query tiles.
+// That kernel is compute-bound (every step feeds 32 queries per wave) and
+// its vector-ALU work competes with the MFMA products for issue, so the
+// per-score vector work is cut down against the shared step:
+//  * masking runs only in the steps that reach tile 0's limit (the
+//    smallest, wave-uniform); each lane then masks against its own limit;
+//  * the reference max moves only when some lane's scaled score passes it by
+//    more than kRescaleSlack -- one compare per lane finds that, and only
+//    then is the max exchanged between the lane groups;
+//  * probabilities are exp2(score * scale_log2 - m) with one fused
+//    multiply-add, and the row sum adds them in float32 (the PV product
+//    takes them rounded to bfloat16; the difference is far below the
+//    output's rounding);
+//  * the masking and the rescale sit in one branch each for all tiles, so
+//    the common path is one straight block the scheduler can interleave.
+template <int NT>
+__device__ __forceinline__ void block_step(const Bf16Path::KV& f, const Bf16Path::QFrag (&qf)[NT],
+                                           SoftmaxState (&sm)[NT], f32x4_t (&acc)[NT][8], int j0,
+                                           const int (&tile_lo)[NT], const int (&lim)[NT],
+                                           float scale_log2, int g) {
+  f32x4_t s[2][NT];
+#pragma unroll
+  for (int kt = 0; kt < 2; ++kt)
+#pragma unroll
+    for (int nt = 0; nt < NT; ++nt) {
+      f32x4_t a = {0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+      for (int st = 0; st < 4; ++st)
+        a = __builtin_amdgcn_mfma_f32_16x16x32_bf16(as_bf16x8(f.k[kt][st]), as_bf16x8(qf[nt].v[st]),
+                                                    a, 0, 0, 0);
+      s[kt][nt] = a;
+    }
+
+  u32x4_t vt[8];
+  transpose_v(f.v, vt);
+
+  float x[NT][8];
+#pragma unroll
+  for (int nt = 0; nt < NT; ++nt)
+#pragma unroll
+    for (int kt = 0; kt < 2; ++kt)
+#pragma unroll
+      for (int r = 0; r < 4; ++r) x[nt][4 * kt + r] = s[kt][nt][r];
+  if (j0 + 32 > tile_lo[0]) {
+#pragma unroll
+    for (int nt = 0; nt < NT; ++nt)
+#pragma unroll
+      for (int kt = 0; kt < 2; ++kt)
+#pragma unroll
+        for (int r = 0; r < 4; ++r)
+          if (j0 + 16 * kt + 4 * g + r >= lim[nt]) x[nt][4 * kt + r] = neg_inf();
+  }
+  float mxs[NT];
+  bool mv[NT];
+  bool any_move = false;
+#pragma unroll
+  for (int nt = 0; nt < NT; ++nt) {
+    // NaN-propagating maximum (v_maximum3_f32): scores are never NaN, and
+    // unlike fmaxf it needs no quieting of the MFMA results first.
+    const float mx = __builtin_elementwise_maximum(
+        __builtin_elementwise_maximum(__builtin_elementwise_maximum(x[nt][0], x[nt][1]), x[nt][2]),
+        __builtin_elementwise_maximum(
+            __builtin_elementwise_maximum(__builtin_elementwise_maximum(x[nt][3], x[nt][4]), x[nt][5]),
+            __builtin_elementwise_maximum(x[nt][6], x[nt][7])));
+    mxs[nt] = mx * scale_log2;
+    mv[nt] = __any(mxs[nt] > sm[nt].m + kRescaleSlack);
+    any_move |= mv[nt];
+  }
+  if (any_move) {
+#pragma unroll
+    for (int nt = 0; nt < NT; ++nt) {
+      if (mv[nt]) {
+        const float m_new = fmaxf(sm[nt].m, max_across_groups(mxs[nt]));
+        const float alpha = (m_new == neg_inf()) ? 1.f : fast_exp2(sm[nt].m - m_new);
+        sm[nt].m = m_new;
+        sm[nt].l *= alpha;
+#pragma unroll
+        for (int t = 0; t < 8; ++t) acc[nt][t] *= alpha;
+      }
+    }
+  }
+#pragma unroll
+  for (int nt = 0; nt < NT; ++nt) {
+    const float neg_m = (sm[nt].m == neg_inf()) ? 0.f : -sm[nt].m;
+    u32x4_t pw;
+    float l = sm[nt].l;
+#pragma unroll
+    for (int e = 0; e < 4; ++e) {
+      const float p0 = fast_exp2(fmaf(x[nt][2 * e], scale_log2, neg_m));
+      const float p1 = fast_exp2(fmaf(x[nt][2 * e + 1], scale_log2, neg_m));
+      pw[e] = pack_bf16x2(p0, p1);
+      l += p0 + p1;
+    }
+    sm[nt].l = l;
+#pragma unroll
+    for (int t = 0; t < 8; ++t)
+      acc[nt][t] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(as_bf16x8(vt[t]), as_bf16x8(pw), acc[nt][t],
+                                                           0, 0, 0);
+  }
+}
+
 // ---------------------------------------------------------------------------
 // Block-masked cross attention of draft training (Sec. 4.1, "Block-wise
 // Attention Mask"): the query at position p sees the target's keys of the
@@ -875,9 +977,8 @@ constexpr int kSharedLds2 = 65536;
 // sequence, 64 * kNT query positions), kNT 16-position tiles per wave (each
 // K/V step read out of LDS once feeds every tile's products), keys streamed
 // through the same LDS ring as the shared-step kernel, workgroups with the
-// most keys first.  The mask is the cross-mode step's own: each lane (query)
-// passes its limit as its tile's prefix length, which the step compares per
-// key.
+// most keys first.  Each lane (query) compares the keys against its own
+// limit, in the steps that reach its tile's limits.
 // ---------------------------------------------------------------------------
 template <int kNT>
 __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(kNT <= 2 ? 2 : 1)))
@@ -897,7 +998,7 @@ void block_attn_kernel(BlockAttnArgs args) {
   const int p_last = min(p0 + kBlockRows - 1, T - 1);
   const int k_end = blk * (p_last / blk);            // the workgroup's largest limit
   const int steps = (k_end + 31) / 32;
-  int p[kNT], my_limit[kNT];
+  int p[kNT], my_limit[kNT], tile_lo[kNT];
   bool live[kNT];
   Bf16Path::QFrag qf[kNT];
 #pragma unroll
@@ -906,11 +1007,11 @@ void block_attn_kernel(BlockAttnArgs args) {
     p[nt] = row0 + c;
     live[nt] = row0 < T;
     my_limit[nt] = p[nt] < T ? blk * (p[nt] / blk) : 0;  // keys [0, limit) are visible
+    tile_lo[nt] = live[nt] ? blk * (row0 / blk) : 0;     // the tile's smallest limit
     load_q<Bf16Path>(qf[nt], (const uint16_t*)args.q + (((size_t)b * T + min(p[nt], T - 1)) * H + h) * kD,
                      p[nt] < T, g);
   }
   const bool any_live = live[0];  // tile 0 of a wave is live whenever tile 1 is
-  const uint64_t anc[kNT] = {};
 
   const size_t head_off = ((size_t)b * H + h) * (size_t)Lcap * kD;
   const char* kslab = (const char*)((const uint16_t*)args.k + head_off);
@@ -918,8 +1019,8 @@ void block_attn_kernel(BlockAttnArgs args) {
 
   const int dma_row = 4 * wave + (lane >> 4);
   const int dma_off = dma_row * 256 + 16 * ((lane & 15) ^ (dma_row & 15));
-  auto issue_step = [&](int t) {
-    char* stage = ring + (t % kStages) * kStepBytes;
+  auto issue_step = [&](int t, int stage_idx) {
+    char* stage = ring + stage_idx * kStepBytes;
     const int j0 = 32 * t;
 #pragma unroll
     for (int k = 0; k < kStepInstr; ++k) {
@@ -931,7 +1032,7 @@ void block_attn_kernel(BlockAttnArgs args) {
     }
   };
 #pragma unroll
-  for (int t = 0; t < kStages - 1; ++t) issue_step(t);
+  for (int t = 0; t < kStages - 1; ++t) issue_step(t, t);
 
   SoftmaxState sm[kNT];
   f32x4_t acc[kNT][8];
@@ -943,19 +1044,27 @@ void block_attn_kernel(BlockAttnArgs args) {
     for (int t = 0; t < 8; ++t) acc[nt][t] = f32x4_t{0.f, 0.f, 0.f, 0.f};
   }
 
-  for (int t = 0; t < steps; ++t) {
-    ring_wait_and_meet<(kStages - 2) * kStepInstr>();
-    issue_step(t + kStages - 1);
-    const int j0 = 32 * t;
-    if (any_live) {
-      Bf16Path::KV f;
-      read_step(f, ring + (t % kStages) * kStepBytes, c, g);
-      if (j0 + 32 > k_end) {
+  // Unrolled over the ring, so every step's stage (and with it each LDS
+  // read's address) is a compile-time offset from per-lane base registers.
+  for (int t0 = 0; t0 < steps; t0 += kStages) {
 #pragma unroll
-        for (int i = 0; i < 8; ++i)
-          if (j0 + Bf16Path::key_slot(g, i) >= k_end) f.v[i] = u32x4_t{0, 0, 0, 0};
+    for (int u = 0; u < kStages; ++u) {
+      const int t = t0 + u;
+      if (t < steps) {
+        ring_wait_and_meet<(kStages - 2) * kStepInstr>();
+        issue_step(t + kStages - 1, (u + kStages - 1) % kStages);
+        const int j0 = 32 * t;
+        if (any_live) {
+          Bf16Path::KV f;
+          read_step(f, ring + u * kStepBytes, c, g);
+          if (j0 + 32 > k_end) {
+#pragma unroll
+            for (int i = 0; i < 8; ++i)
+              if (j0 + Bf16Path::key_slot(g, i) >= k_end) f.v[i] = u32x4_t{0, 0, 0, 0};
+          }
+          block_step<kNT>(f, qf, sm, acc, j0, tile_lo, my_limit, args.scale_log2, g);
+        }
       }
-      step<kNT, false, true>(f, qf, sm, acc, j0, 0, k_end, 64, anc, args.scale_log2, g, my_limit);
     }
   }
   asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
