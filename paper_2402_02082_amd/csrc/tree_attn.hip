@@ -1027,8 +1027,11 @@ void block_attn_kernel(BlockAttnArgs args) {
       const int m = k / 2, hi = k & 1;
       const __amdgpu_buffer_rsrc_t rs = step_rsrc(m ? vslab : kslab, j0, k_end, 256);
       char* dst = stage + m * (kStepBytes / 2) + (wave + 4 * hi) * 1024;
+      // default cache policy: every K/V row is read again by the workgroups
+      // of the head's later query blocks, and the non-temporal hint of the
+      // decode kernels (1.5x the HBM reads here) would evict it from L2
       __builtin_amdgcn_raw_ptr_buffer_load_lds(rs, (lds_ptr_t)dst, 16, dma_off + 4096 * hi, 0, 0,
-                                               kStream);
+                                               kKeep);
     }
   };
 #pragma unroll
