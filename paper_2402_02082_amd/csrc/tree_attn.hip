@@ -266,23 +266,27 @@ struct SoftmaxState {
 
 // Given the raw scores x[] of this lane's keys for one query tile (masked
 // ones -inf), decide whether the wave moves its reference max, rescale if so,
-// and turn x[] into probabilities exp2(x * scale_log2 - m).  The max is taken
-// over the rounded scaled scores themselves, so the largest score of a row
-// gets probability exactly 1.  Returns true when the accumulators must be
-// rescaled by `alpha`.
+// and turn x[] into probabilities exp2(x * scale_log2 - m).  The decision
+// needs no exchange between lanes: the reference moves when some lane's
+// largest scaled score passes it by more than kRescaleSlack, and only then
+// is the max taken over the column's lane groups.  The max is taken over the
+// rounded scaled scores themselves, so the largest score of a row gets
+// probability exactly 1 when it sets the reference.  Returns true when the
+// accumulators must be rescaled by `alpha`.
 template <int NV>
 __device__ __forceinline__ bool softmax_update(float (&x)[NV], SoftmaxState& st, float scale_log2,
                                                float& alpha) {
 #pragma unroll
   for (int i = 0; i < NV; ++i) x[i] *= scale_log2;
+  // NaN-propagating maximum (v_maximum3_f32): scores are never NaN, and
+  // unlike fmaxf it needs no quieting of the MFMA results first.
   float mx = x[0];
 #pragma unroll
-  for (int i = 1; i < NV; ++i) mx = fmaxf(mx, x[i]);
-  mx = max_across_groups(mx);
+  for (int i = 1; i < NV; ++i) mx = __builtin_elementwise_maximum(mx, x[i]);
   const bool move = __any(mx > st.m + kRescaleSlack);
   alpha = 1.f;
   if (move) {
-    const float m_new = fmaxf(st.m, mx);
+    const float m_new = fmaxf(st.m, max_across_groups(mx));
     alpha = (m_new == neg_inf()) ? 1.f : fast_exp2(st.m - m_new);
     st.m = m_new;
     st.l *= alpha;
@@ -361,7 +365,7 @@ __device__ __forceinline__ void step(const Bf16Path::KV& f, const Bf16Path::QFra
 #pragma unroll
     for (int e = 0; e < 4; ++e) {
       pw[e] = pack_bf16x2(x[2 * e], x[2 * e + 1]);
-      psum += bf16_lo(pw[e]) + bf16_hi(pw[e]);
+      psum += x[2 * e] + x[2 * e + 1];
     }
     sm[nt].l += psum;
 #pragma unroll
