@@ -26,7 +26,8 @@
 //                    (each lane holds 16 contiguous bytes of one key row),
 //                    B = the resident Q fragments;
 //   online softmax on S^T: the output layout puts one query per lane column,
-//                    so the running max/sum are per-lane scalars and only the
+//                    so the running max/sum are per-lane scalars; the
+//                    reference max moves lazily, and only when it moves do the
 //                    four 16-lane groups exchange their max (two row swaps);
 //   O^T[d, query] += V^T P^T  on the same instruction, A = V^T built in
 //                    registers: each lane holds 16 contiguous bytes (8 head
