@@ -993,8 +993,27 @@ void block_attn_kernel(BlockAttnArgs args) {
   constexpr int kBlockRows = 16 * kNT * kWaves;  // query positions per workgroup
   __shared__ __attribute__((aligned(1024))) char ring[kSharedLds4];
 
-  const int h = blockIdx.x, b = blockIdx.y;
-  const int p0 = (gridDim.z - 1 - blockIdx.z) * kBlockRows;  // most keys first
+  // Dispatch order.  Workgroups go to the eight XCDs round-robin by linear
+  // id, and each XCD has its own L2.  All query blocks of a (sequence, head)
+  // pair are mapped to one XCD, and each XCD takes its pairs four at a time,
+  // every query block of the four (most keys first) before the next four:
+  // the blocks of a pair start together and stream the same K/V rows in
+  // step, while the order over blocks stays longest first.  (Any dispatch
+  // order gives the same results; this one only keeps reuse in L2.)
+  const int P = gridDim.x * gridDim.y, Z = gridDim.z;
+  const int lin = blockIdx.x + gridDim.x * (blockIdx.y + gridDim.y * blockIdx.z);
+  int pair, zi;
+  if (P % 32 == 0) {
+    const int x = lin % 8, k = lin / 8;
+    const int grp = k / (4 * Z), r = k % (4 * Z);
+    zi = r / 4;
+    pair = (4 * grp + r % 4) * 8 + x;
+  } else {
+    pair = blockIdx.x + gridDim.x * blockIdx.y;
+    zi = blockIdx.z;
+  }
+  const int h = pair % args.H, b = pair / args.H;
+  const int p0 = (Z - 1 - zi) * kBlockRows;  // most keys first
   const int tid = threadIdx.x, lane = tid & 63;
   const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
   const int c = lane & 15, g = lane >> 4;
