@@ -117,7 +117,8 @@ size_t glide_tree_attn_workspace(int B, int N, int H, int D, int L_cap,
  *   tree_parents [B, N] int32 or NULL (cross mode).
  *   out          [B, N, H, D]  dtype; may not alias the inputs.  Rows of a
  *                sequence with no visible key (cross mode, L_b = 0) are 0.
- *   B >= 1; 1 <= N <= 64; H >= 1; D == 128; L_cap >= N (tree) or >= 1.
+ *   1 <= B <= 65535; 1 <= N <= 64; H >= 1; B * N * H < 2^31; D == 128;
+ *   N (tree) or 1 <= L_cap <= 4194304 (2^22).
  *   dtype        GLIDE_BF16 or GLIDE_F32.
  *   scale        softmax scale; <= 0 selects 1/sqrt(D).
  *   max_splits   0 = choose automatically, else 1..64 key-range splits.
@@ -217,8 +218,9 @@ int tree_verify(const int32_t* target_argmax, const int32_t* cand_tokens,
  *   accept_len    [B] int32 out; last_node, bonus [B] and path [B, N]
  *                 (accepted node at depth d + 1 in slot d, -1 after) int32
  *                 out, nullable.
- *   B <= 65535; 1 <= N <= 64; D == 128; L_cap >= N; seq_lens[b] + N <=
- *   L_cap (clamped into range unless GLIDE_VALIDATE=1).
+ *   B <= 65535; 1 <= N <= 64; B * N * H < 2^31; D == 128;
+ *   N <= L_cap <= 4194304; seq_lens[b] + N <= L_cap (clamped into range
+ *   unless GLIDE_VALIDATE=1).
  * Two launches (the argmax, then the acceptance and copy); no workspace.
  */
 int glide_verify_commit(const float* logits, int V, const int32_t* cand_tokens,
@@ -330,7 +332,8 @@ int spec_sample_verify(const int32_t* draft_tokens, const float* draft_probs,
  * and gets zeros.  bfloat16 in and out, float32 accumulation.
  *   q   [B, T, H, D] (the draft's projected queries of a training sequence);
  *   k_cache, v_cache [B, H, L_cap, D] holding positions 0 .. T - 1;
- *   out [B, T, H, D].  D == 128; 1 <= T <= L_cap; block >= 1; B <= 65535;
+ *   out [B, T, H, D].  D == 128; 1 <= T <= L_cap <= 4194304; block >= 1;
+ *   B <= 65535; B * H * ceil(T / 64) < 2^31;
  *   scale <= 0 means 1/sqrt(D).
  */
 int glide_block_attn(const void* q, const void* k_cache, const void* v_cache, void* out, int B,

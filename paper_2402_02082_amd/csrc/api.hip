@@ -48,11 +48,17 @@ bool parents_ok(const std::vector<int32_t>& parents, int B, int N) {
   return true;
 }
 
+// Kernels keep key-row byte offsets inside one (sequence, head) slab in
+// 32-bit registers (buffer descriptors: rows * 512 bytes for float32), and
+// the split merge counts its output rows B * N * H in an int.
+constexpr int kMaxKeys = 1 << 22;
+
 bool tree_attn_sizes_ok(int B, int N, int H, int D, int L_cap, bool tree) {
   if (B < 1 || B > 65535 || H < 1 || N < 1 || N > glide::kMaxNodes) return false;  // B is a grid dim
   if (D != glide::kHeadDim) return false;
-  if (L_cap < (tree ? N : 1)) return false;
-  // keep every element offset inside size_t and every key index inside int
+  if (L_cap < (tree ? N : 1) || L_cap > kMaxKeys) return false;
+  if ((double)B * N * H > 2147483647.0) return false;
+  // keep every element offset inside size_t
   if ((double)B * H * (double)L_cap * D > 9.0e18) return false;
   return true;
 }
@@ -333,7 +339,8 @@ int glide_block_attn(const void* q, const void* k_cache, const void* v_cache, vo
   if (!q || !k_cache || !v_cache || !out) return GLIDE_EINVAL;
   if (B < 1 || B > 65535 || H < 1 || T < 1 || T > L_cap || D != glide::kHeadDim || block < 1)
     return GLIDE_EINVAL;
-  if ((T + 63) / 64 > 65535 || !isfinite(scale)) return GLIDE_EINVAL;
+  if ((T + 63) / 64 > 65535 || L_cap > kMaxKeys || !isfinite(scale)) return GLIDE_EINVAL;
+  if ((double)B * H * ((T + 63) / 64) > 2147483647.0) return GLIDE_EINVAL;  // linear workgroup ids
   if ((double)B * H * (double)L_cap * D > 9.0e18 || (double)B * T * H * D > 9.0e18) return GLIDE_EINVAL;
   glide::BlockAttnArgs a{};
   a.q = q;

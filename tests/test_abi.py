@@ -59,6 +59,7 @@ def _attn(lib, **kw):
     dict(N=0), dict(N=65), dict(D=64), dict(D=256), dict(B=0), dict(H=0), dict(dtype=2),
     dict(dtype=-1), dict(L_cap=15), dict(splits=-1), dict(splits=65),
     dict(scale=float("nan")), dict(scale=float("inf")), dict(ws=None), dict(ws_bytes=16),
+    dict(L_cap=(1 << 22) + 1), dict(B=65536), dict(B=65535, N=64, H=1024),
 ])
 def test_tree_attn_rejects(lib, bad):
     assert _attn(lib, **bad) == glide.GLIDE_EINVAL
@@ -264,6 +265,7 @@ def _blk(lib, **kw):
 @pytest.mark.parametrize("bad", [
     dict(q=None), dict(k=None), dict(v=None), dict(out=None), dict(B=0), dict(B=65536), dict(T=0),
     dict(T=2049), dict(H=0), dict(D=64), dict(block=0), dict(scale=float("inf")),
+    dict(L_cap=(1 << 22) + 1, T=4096), dict(B=65535, H=1024, T=4096, L_cap=4096),
 ])
 def test_block_attn_rejects(lib, bad):
     assert _blk(lib, **bad) == glide.GLIDE_EINVAL
