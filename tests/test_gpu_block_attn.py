@@ -61,3 +61,17 @@ def test_two_tile_launch_sampled():
     err, got = _run(11, 1, T, H, T, 5, positions=pos)
     assert err <= BF16_TOL, err
     assert np.all(got[:, :5] == 0)
+
+
+def test_bench_shape_sampled():
+    """The benchmark's shape and launch (4 sequences x 2048 positions, 32
+    heads, blocks of 5: two tiles per wave, every query block of a (sequence,
+    head) pair on one XCD, four pairs at a time): sampled positions in the
+    first, middle and last query blocks against the oracle."""
+    require_gpu()
+    B, T, H = 4, 2048, 32
+    pos = sorted({0, 5, 127, 128, 1000, 1024, 1919, 1920, 2040, 2047})
+    say("block_attn bench shape", dict(B=B, T=T, H=H, positions=len(pos)))
+    err, got = _run(13, B, T, H, T, 5, positions=pos)
+    assert err <= BF16_TOL, err
+    assert np.all(got[:, :5] == 0)
