@@ -21,7 +21,7 @@ from oracle import attention as OA
 from oracle import cape as OC
 from oracle import verify as OV
 from synth import workloads as W
-from tests.gpu_common import BF16_TOL, require_gpu, say, to64
+from tests.gpu_common import BF16_TOL, F32_TOL, require_gpu, say, to64
 
 pytestmark = pytest.mark.gpu
 
@@ -125,3 +125,37 @@ def test_attention(cfg):
                     assert err <= BF16_TOL, ("cross", b, h, err)
         del q, k, v, out
         torch.cuda.empty_cache()
+
+
+@pytest.mark.parametrize("cfg", [1, 2, 3])
+def test_attention_f32(cfg):
+    """The float32 mode on the same values (the workload's bf16 draws widened
+    exactly), first layer, automatic split plan: sampled outputs against the
+    float64 oracle within 1e-5."""
+    require_gpu()
+    wl = W.WORKLOADS[cfg]
+    dev = torch.device("cuda")
+    lens_np = W.prefix_lengths(wl, SEED)
+    lens = torch.from_numpy(lens_np).to(dev)
+    if wl.tree == "cape":
+        probs, _, _ = W.draft_probs(wl, SEED)
+        _, par_gpu, _ = _gpu_tree(wl, probs, wl.k)
+        _, par_or, _ = OC.cape_expand(probs, wl.k, wl.nodes)
+        assert np.array_equal(par_gpu.cpu().numpy(), par_or)
+    else:
+        par_or = np.tile(np.arange(-1, wl.nodes - 1, dtype=np.int32), (wl.batch, 1))
+        par_gpu = torch.from_numpy(par_or).to(dev)
+    say("attention f32", wl.name)
+    q, k, v = (t.float() for t in W.attention_layer(wl, SEED, 0, torch.bfloat16, dev))
+    out = torch.full_like(q, float("nan"))
+    glide.glide_tree_attn(q, k, v, lens, par_gpu, out)
+    torch.cuda.synchronize()
+    nodes = _sample_nodes(wl.nodes, wl.depth)
+    for b in sorted({0, wl.batch - 1}):
+        for h in sorted({0, wl.heads // 2, wl.heads - 1}):
+            L = int(lens_np[b])
+            rows = L + wl.nodes
+            ref = OA.tree_attention_head(to64(q[b, :, h]), to64(k[b, h, :rows]), to64(v[b, h, :rows]),
+                                         L, par_or[b], nodes=nodes)
+            err = float(np.abs(to64(out[b, :, h])[nodes] - ref[nodes]).max())
+            assert err <= F32_TOL, (b, h, err)
