@@ -432,6 +432,26 @@ __device__ __forceinline__ void store_2(uint16_t* dst, float a, float b) {
 
 __device__ __forceinline__ void store_2(float* dst, float a, float b) { *(float2*)dst = make_float2(a, b); }
 
+// Sequence taken by workgroup row y.  When every workgroup covers a whole
+// sequence (one split) and 2 <= B <= 64, the y-th longest (ties to the lower
+// index): the grid, dispatched in linear order, then starts the longest
+// sequences' workgroups first, on CUs of their own, and the shortest ones
+// share CUs -- longest-first scheduling, which shortens the ragged tail
+// (33B and long-context shapes: -6 %).  Otherwise sequence y.  Ranks of
+// raw lengths form a permutation, so every sequence is still taken exactly
+// once and the results do not depend on the order.
+__device__ __forceinline__ int seq_of_row(const int32_t* seq_lens, int B, int splits, int y, int lane) {
+  if (splits != 1 || B < 2 || B > 64) return y;
+  const int len = lane < B ? seq_lens[lane] : 0;
+  int rank = 0;
+  for (int j = 0; j < B; ++j) {
+    const int lj = __shfl(len, j);
+    rank += (lj > len) || (lj == len && j < lane);
+  }
+  const uint64_t hit = __ballot(lane < B && rank == y);
+  return __builtin_amdgcn_readfirstlane(__ffsll((long long)hit) - 1);
+}
+
 // Work of one wave: the query tiles it owns and the key steps it takes.
 // QG query groups split the 16-row query tiles; the 4 / QG waves of a group
 // interleave the key steps of the split, so each K/V step is loaded by one
@@ -458,8 +478,9 @@ void tree_attn_kernel(AttnArgs args) {
   constexpr int kWpg = Task::kWavesPerGroup;
   constexpr int kStride = Task::kStride;
 
-  const int h = blockIdx.x, b = blockIdx.y, s = blockIdx.z;
   const int tid = threadIdx.x, lane = tid & 63;
+  const int h = blockIdx.x, s = blockIdx.z;
+  const int b = seq_of_row(args.seq_lens, args.B, args.splits, blockIdx.y, lane);
   const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
   const int c = lane & 15, g = lane >> 4;
   const int qg = wave / kWpg, wig = wave % kWpg;  // query group, wave in group
@@ -680,8 +701,9 @@ void tree_attn_shared_kernel(AttnArgs args) {
   static_assert(kStages >= 2 * kWpt && kStages * kStepBytes == LDS_BYTES, "ring of two rounds or more");
   __shared__ __attribute__((aligned(1024))) char ring[LDS_BYTES];
 
-  const int h = blockIdx.x, b = blockIdx.y, s = blockIdx.z;
   const int tid = threadIdx.x, lane = tid & 63;
+  const int h = blockIdx.x, s = blockIdx.z;
+  const int b = seq_of_row(args.seq_lens, args.B, args.splits, blockIdx.y, lane);
   const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
   const int c = lane & 15, g = lane >> 4;
   const int tile = wave % TQ, phase = wave / TQ;
