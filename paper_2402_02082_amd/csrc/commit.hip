@@ -4,15 +4,18 @@
 // after a verification step only the accepted tokens' cache rows are kept;
 // Sec. 4.2: a tree candidate is accepted when its whole root path is.
 //
-// One wave per (sequence, layer, head).  Every wave first works out its
-// sequence's acceptance (one lane per node, ancestor masks by pointer
-// doubling -- a few dozen instructions, cheaper than a second launch), then
-// moves the accepted path's K and V rows of its (layer, head) slab to the
-// rows right behind the prefix.  The path's node at depth d + 1 sits at row
-// L + n_{d+1} >= L + d, so a destination row is never the source of a deeper
-// slot; all sources of a batch are loaded before its stores, so a
-// destination that is the source of a shallower slot is read first.  Each
-// slab is moved by exactly one wave.
+// Workgroups of four waves, a few hundred in all: each sequence's (layer,
+// head) slabs are dealt out in contiguous ranges to its workgroups and
+// round-robin to their waves.  Every wave first works out its sequence's
+// acceptance (one lane per node, ancestor masks by pointer doubling -- a few
+// dozen instructions, cheaper than a second launch), then moves the accepted
+// path's K and V rows of each of its slabs to the rows right behind the
+// prefix, 16 loads per matrix in flight across slabs.  The path's node at
+// depth d + 1 sits at row L + n_{d+1} >= L + d, so a destination row is never
+// the source of a deeper slot; a slab's slots are visited in order and all
+// sources of a batch are loaded before its stores, so a destination that is
+// the source of a shallower slot is read first.  Each slab is moved by
+// exactly one wave.
 #include <hip/hip_runtime.h>
 #include <stdint.h>
 
@@ -41,10 +44,9 @@ __device__ __forceinline__ uint64_t wave_max_u64(uint64_t v) {
   return v;
 }
 
-__global__ __launch_bounds__(64 * kWaves) void verify_commit_kernel(CommitArgs args) {
-  const int b = blockIdx.z, layer = blockIdx.y;
+__global__ __launch_bounds__(64 * kWaves) void verify_commit_kernel(CommitArgs args, int slabs_per_wg) {
+  const int b = blockIdx.y;
   const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
-  const int h = blockIdx.x * kWaves + wave;
   const int N = args.N;
   const int32_t* ta = args.target_argmax + (size_t)b * (N + 1);
 
@@ -81,7 +83,7 @@ __global__ __launch_bounds__(64 * kWaves) void verify_commit_kernel(CommitArgs a
   __shared__ int node_of[kWaves][64];
   if (on_path) node_of[wave][rank] = lane;
 
-  if (blockIdx.x == 0 && layer == 0 && wave == 0) {
+  if (blockIdx.x == 0 && wave == 0) {
     if (lane == 0) {
       args.accept_len[b] = a;
       args.seq_lens_out[b] = args.seq_lens[b] + a;
@@ -94,35 +96,51 @@ __global__ __launch_bounds__(64 * kWaves) void verify_commit_kernel(CommitArgs a
     }
   }
   __syncthreads();
-  if (layer >= args.layers || h >= args.H || a == 0) return;
+  if (a == 0 || args.layers == 0) return;
 
-  const int R = args.row_bytes;                 // 256 (bf16) or 512 (fp32)
+  const int H = args.H, R = args.row_bytes;     // 256 (bf16) or 512 (fp32)
   const int lanes_per_row = R / 16;
   const int rows_per_load = 64 / lanes_per_row;
   const int chunk = lane % lanes_per_row, q = lane / lanes_per_row;
   const int L = min(max(args.seq_lens[b], 0), args.L_cap - N);
-  const size_t slab = (((size_t)b * args.H + h) * args.L_cap + L) * R + chunk * 16;
-  char* kb = args.k[layer] + slab;
-  char* vb = args.v[layer] + slab;
+  const int s_begin = blockIdx.x * slabs_per_wg;
+  const int s_end = min(args.layers * H, s_begin + slabs_per_wg);
+  const int mine = s_end > s_begin + wave ? (s_end - s_begin - wave + kWaves - 1) / kWaves : 0;
+  const int upr = (a + rows_per_load - 1) / rows_per_load;  // load units per slab
+  const int units = mine * upr;
 
-  for (int s0 = 0; s0 < a; s0 += kIter * rows_per_load) {
+  // unit u: slab s_begin + wave + kWaves * (u / upr), slots (u % upr) *
+  // rows_per_load .. + rows_per_load - 1 (this lane: + q)
+  for (int u0 = 0; u0 < units; u0 += kIter) {
     u32x4_t kx[kIter], vx[kIter];
 #pragma unroll
     for (int i = 0; i < kIter; ++i) {
-      const int d = s0 + i * rows_per_load + q;
-      const int n = d < a ? node_of[wave][d] : d;
-      if (n != d) {  // a path that starts down the chain keeps those rows in place
-        kx[i] = *(const u32x4_t*)(kb + (size_t)n * R);
-        vx[i] = *(const u32x4_t*)(vb + (size_t)n * R);
+      const int u = u0 + i;
+      if (u < units) {
+        const int sl = s_begin + wave + kWaves * (u / upr);
+        const int d = (u % upr) * rows_per_load + q;
+        const int n = d < a ? node_of[wave][d] : d;
+        if (n != d) {  // a path that starts down the chain keeps those rows in place
+          const int layer = sl / H, h = sl % H;
+          const size_t slab = (((size_t)b * H + h) * args.L_cap + L) * R + chunk * 16;
+          kx[i] = *(const u32x4_t*)(args.k[layer] + slab + (size_t)n * R);
+          vx[i] = *(const u32x4_t*)(args.v[layer] + slab + (size_t)n * R);
+        }
       }
     }
 #pragma unroll
     for (int i = 0; i < kIter; ++i) {
-      const int d = s0 + i * rows_per_load + q;
-      const int n = d < a ? node_of[wave][d] : d;
-      if (n != d) {
-        *(u32x4_t*)(kb + (size_t)d * R) = kx[i];
-        *(u32x4_t*)(vb + (size_t)d * R) = vx[i];
+      const int u = u0 + i;
+      if (u < units) {
+        const int sl = s_begin + wave + kWaves * (u / upr);
+        const int d = (u % upr) * rows_per_load + q;
+        const int n = d < a ? node_of[wave][d] : d;
+        if (n != d) {
+          const int layer = sl / H, h = sl % H;
+          const size_t slab = (((size_t)b * H + h) * args.L_cap + L) * R + chunk * 16;
+          *(u32x4_t*)(args.k[layer] + slab + (size_t)d * R) = kx[i];
+          *(u32x4_t*)(args.v[layer] + slab + (size_t)d * R) = vx[i];
+        }
       }
     }
   }
@@ -133,8 +151,12 @@ __global__ __launch_bounds__(64 * kWaves) void verify_commit_kernel(CommitArgs a
 hipError_t launch_verify_commit(const float* logits, int V, const CommitArgs& a, hipStream_t stream) {
   hipError_t e = launch_argmax_rows(logits, a.B * (a.N + 1), V, a.target_argmax, stream);
   if (e != hipSuccess) return e;
-  const dim3 grid((a.H + kWaves - 1) / kWaves, a.layers > 0 ? a.layers : 1, a.B);
-  hipLaunchKernelGGL(verify_commit_kernel, grid, dim3(64 * kWaves), 0, stream, a);
+  // about 512 workgroups in all, each sequence's slabs in equal ranges
+  const int slabs = a.layers * a.H;
+  const int want = max(1, min(slabs, (512 + a.B - 1) / a.B));
+  const int per_wg = slabs > 0 ? (slabs + want - 1) / want : 0;
+  const int groups = per_wg > 0 ? (slabs + per_wg - 1) / per_wg : 1;
+  hipLaunchKernelGGL(verify_commit_kernel, dim3(groups, a.B), dim3(64 * kWaves), 0, stream, a, per_wg);
   return hipGetLastError();
 }
 
