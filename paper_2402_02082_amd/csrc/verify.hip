@@ -3,9 +3,12 @@
 // when it equals the target's greedy token; Sec. 4.2 verifies the whole
 // expanded proposal in one pass; Sec. 5.1 uses greedy acceptance for CaPE).
 //
-//   argmax_rows   one 1024-thread workgroup per logits row: the first index
-//                 of the row maximum (a max over (order-preserving value,
-//                 ~index) keys).
+//   argmax_rows   one workgroup per logits row: the first index of the row
+//                 maximum (a max over (order-preserving value, ~index)
+//                 keys); 1024 threads while every row's workgroup fits on
+//                 the chip at once (a 32000-entry row is one round of
+//                 loads), 256 beyond that, so that no rows wait for a
+//                 second round of workgroups.
 //   tree_verify   one wave per sequence, one lane per node: a node is
 //                 accepted iff every node on its root path matches, i.e. its
 //                 ancestor-or-self bitmask has no non-matching bit; the
@@ -47,11 +50,12 @@ __device__ __forceinline__ uint64_t wave_max_u64(uint64_t v) {
   return v;
 }
 
-// One 1024-thread workgroup per row; each thread requests 8 float4 (32
-// values) at once, so a 32000-entry row is a single round of loads.
-constexpr int kArgmaxThreads = 1024;
+// One workgroup of kThreads per row; each thread requests 8 float4 (32
+// values) at once, so with 1024 threads a 32000-entry row is a single round
+// of loads.
 constexpr int kArgmaxVec = 8;
 
+template <int kArgmaxThreads>
 __global__ __launch_bounds__(kArgmaxThreads) void argmax_rows_kernel(const float* __restrict__ logits,
                                                                      int V, int32_t* __restrict__ idx) {
   const int row = blockIdx.x, tid = threadIdx.x;
@@ -144,7 +148,11 @@ __global__ __launch_bounds__(64) void tree_verify_kernel(const int32_t* __restri
 
 hipError_t launch_argmax_rows(const float* logits, int rows, int V, int32_t* idx,
                               hipStream_t stream) {
-  hipLaunchKernelGGL(argmax_rows_kernel, dim3(rows), dim3(kArgmaxThreads), 0, stream, logits, V, idx);
+  // two 1024-thread workgroups fit on a CU
+  if (rows <= 2 * kNumCU)
+    hipLaunchKernelGGL(argmax_rows_kernel<1024>, dim3(rows), dim3(1024), 0, stream, logits, V, idx);
+  else
+    hipLaunchKernelGGL(argmax_rows_kernel<256>, dim3(rows), dim3(256), 0, stream, logits, V, idx);
   return hipGetLastError();
 }
 

@@ -119,6 +119,19 @@ def test_argmax_rows(V):
     assert np.array_equal(gpu_argmax(x), OV.argmax_rows(x))
 
 
+@pytest.mark.parametrize("V", [1001, 32000])
+def test_argmax_many_rows(V):
+    """More rows than two 1024-thread workgroups per CU hold (the 256-thread
+    launch), ties and signed zeros included."""
+    require_gpu()
+    rng = np.random.default_rng(V + 7)
+    x = rng.integers(-3, 3, size=(600, V)).astype(np.float32)
+    x[5] = f32(-0.0)
+    x[599, :] = -np.inf
+    say("argmax many rows", V)
+    assert np.array_equal(gpu_argmax(x), OV.argmax_rows(x))
+
+
 def gpu_verify(ta, cand, parents):
     dev = torch.device("cuda")
     B, N = cand.shape
