@@ -81,6 +81,11 @@ CASES = [
     (2, 5, 3, [31, 129], None, 2),
     (1, 64, 2, [3000], None, 0),
     (3, 8, 2, [0, 33, 64], None, 1),    # empty key set for b = 0
+    # one split per sequence: workgroup rows take the sequences longest first
+    # (B <= 64, ties among equal lengths) or in order (B > 64)
+    (64, 16, 1, [(37 * i) % 300 for i in range(64)], "cape", 1),
+    (5, 32, 2, [90, 300, 90, 0, 300], "random", 1),
+    (70, 5, 1, [(53 * i) % 200 for i in range(70)], None, 1),
 ]
 
 
