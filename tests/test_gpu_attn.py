@@ -191,3 +191,40 @@ def test_validation_reports_bad_device_data(monkeypatch):
     glide.glide_tree_attn(q, k, k, lens, torch.tensor([[-1, 0, 1, 1]], dtype=torch.int32,
                                                        device=dev), out)
     torch.cuda.synchronize()
+
+
+@pytest.mark.parametrize("dtype", [torch.bfloat16, torch.float32], ids=["bf16", "f32"])
+@pytest.mark.parametrize("N,kind", [(16, "cape"), (64, "random"), (5, None)])
+def test_peaked_scores(N, kind, dtype):
+    """Queries scaled by 24 (scaled scores with a spread of hundreds in log2
+    units): the lazily moved reference max is passed by far, often, and by
+    single keys deep in the sequence; outputs stay within the tolerance."""
+    require_gpu()
+    B, H = 2, 3
+    lens = [1500, 700]
+    tree = kind is not None
+    L_cap = max(lens) + (N if tree else 0)
+    say("tree_attn peaked", dict(N=N, kind=kind, dtype=str(dtype)))
+    q = (cpu_normal((B, N, H, D), 31, torch.float32) * 24).to(dtype)
+    k = cpu_normal((B, H, L_cap, D), 32, dtype)
+    v = cpu_normal((B, H, L_cap, D), 33, dtype)
+    parents = _parents(kind, B, N, 34)
+    dev = torch.device("cuda")
+    out = torch.full((B, N, H, D), float("nan"), dtype=dtype, device=dev)
+    glide.glide_tree_attn(q.to(dev), k.to(dev), v.to(dev), torch.tensor(lens, dtype=torch.int32, device=dev),
+                          None if parents is None else torch.from_numpy(parents).to(dev), out)
+    torch.cuda.synchronize()
+    ref = OA.tree_attention(to64(q), to64(k), to64(v), lens, parents)
+    # A peaked softmax returns nearly single value rows (|v| up to ~4), not
+    # averages: in bf16 the probabilities and the output are rounded to 8
+    # significant bits, so the bound is 1e-2 + 2^-8 |ref| (one output rounding
+    # of a value in [4, 8) alone is up to 0.016).  float32 rounding of a score
+    # is relative to its size, so the float32 bound scales with the query
+    # scale.
+    got = to64(out)
+    if dtype == torch.bfloat16:
+        excess = np.abs(got - ref) - (BF16_TOL + np.abs(ref) / 256)
+        assert float(excess.max()) <= 0, float(np.abs(got - ref).max())
+    else:
+        err = float(np.abs(got - ref).max())
+        assert err <= 24 * F32_TOL, err
