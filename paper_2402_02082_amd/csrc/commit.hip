@@ -105,42 +105,60 @@ __global__ __launch_bounds__(64 * kWaves) void verify_commit_kernel(CommitArgs a
   const int L = min(max(args.seq_lens[b], 0), args.L_cap - N);
   const int s_begin = blockIdx.x * slabs_per_wg;
   const int s_end = min(args.layers * H, s_begin + slabs_per_wg);
-  const int mine = s_end > s_begin + wave ? (s_end - s_begin - wave + kWaves - 1) / kWaves : 0;
+  const int w = __builtin_amdgcn_readfirstlane(wave);
+  const int mine = s_end > s_begin + w ? (s_end - s_begin - w + kWaves - 1) / kWaves : 0;
   const int upr = (a + rows_per_load - 1) / rows_per_load;  // load units per slab
-  const int units = mine * upr;
 
-  // unit u: slab s_begin + wave + kWaves * (u / upr), slots (u % upr) *
-  // rows_per_load .. + rows_per_load - 1 (this lane: + q)
-  for (int u0 = 0; u0 < units; u0 += kIter) {
-    u32x4_t kx[kIter], vx[kIter];
-#pragma unroll
-    for (int i = 0; i < kIter; ++i) {
-      const int u = u0 + i;
-      if (u < units) {
-        const int sl = s_begin + wave + kWaves * (u / upr);
-        const int d = (u % upr) * rows_per_load + q;
-        const int n = d < a ? node_of[wave][d] : d;
-        if (n != d) {  // a path that starts down the chain keeps those rows in place
-          const int layer = sl / H, h = sl % H;
-          const size_t slab = (((size_t)b * H + h) * args.L_cap + L) * R + chunk * 16;
-          kx[i] = *(const u32x4_t*)(args.k[layer] + slab + (size_t)n * R);
-          vx[i] = *(const u32x4_t*)(args.v[layer] + slab + (size_t)n * R);
-        }
+  // Units in order: this wave's j-th slab s_begin + w + kWaves * j, its rows
+  // rg * rows_per_load .. + rows_per_load - 1 (this lane: + q).  The cursor
+  // (j, rg, layer, h) is wave-uniform and advances without divisions; each
+  // batch replays it for the stores.
+  struct Cursor {
+    int j, rg, layer, h;
+  };
+  Cursor cur{0, 0, (s_begin + w) / H, (s_begin + w) % H};
+  auto advance = [&](Cursor& c) {
+    if (++c.rg == upr) {
+      c.rg = 0;
+      ++c.j;
+      c.h += kWaves;
+      while (c.h >= H) {
+        c.h -= H;
+        ++c.layer;
       }
     }
+  };
+  auto row_offset = [&](const Cursor& c) {
+    return (((size_t)b * H + c.h) * args.L_cap + L) * R + chunk * 16;
+  };
+  while (cur.j < mine) {
+    u32x4_t kx[kIter], vx[kIter];
+    const Cursor start = cur;
 #pragma unroll
     for (int i = 0; i < kIter; ++i) {
-      const int u = u0 + i;
-      if (u < units) {
-        const int sl = s_begin + wave + kWaves * (u / upr);
-        const int d = (u % upr) * rows_per_load + q;
+      if (cur.j < mine) {
+        const int d = cur.rg * rows_per_load + q;
+        const int n = d < a ? node_of[wave][d] : d;
+        if (n != d) {  // a path that starts down the chain keeps those rows in place
+          const size_t off = row_offset(cur) + (size_t)n * R;
+          kx[i] = *(const u32x4_t*)(args.k[cur.layer] + off);
+          vx[i] = *(const u32x4_t*)(args.v[cur.layer] + off);
+        }
+        advance(cur);
+      }
+    }
+    Cursor st = start;
+#pragma unroll
+    for (int i = 0; i < kIter; ++i) {
+      if (st.j < mine) {
+        const int d = st.rg * rows_per_load + q;
         const int n = d < a ? node_of[wave][d] : d;
         if (n != d) {
-          const int layer = sl / H, h = sl % H;
-          const size_t slab = (((size_t)b * H + h) * args.L_cap + L) * R + chunk * 16;
-          *(u32x4_t*)(args.k[layer] + slab + (size_t)d * R) = kx[i];
-          *(u32x4_t*)(args.v[layer] + slab + (size_t)d * R) = vx[i];
+          const size_t off = row_offset(st) + (size_t)d * R;
+          *(u32x4_t*)(args.k[st.layer] + off) = kx[i];
+          *(u32x4_t*)(args.v[st.layer] + off) = vx[i];
         }
+        advance(st);
       }
     }
   }
