@@ -132,7 +132,7 @@ int glide_tree_attn(const void* q, const void* k_cache, const void* v_cache,
                     void* workspace, size_t ws_bytes, hipStream_t stream);
 
 /* Workspace bytes cape_expand needs (the best candidates of every 4096-token
- * part of every draft row); 0 for invalid sizes. */
+ * part of every draft row); 0 for invalid sizes (as cape_expand rejects). */
 size_t cape_expand_workspace(int B, int gamma, int V);
 
 /*
@@ -154,7 +154,8 @@ size_t cape_expand_workspace(int B, int gamma, int V);
  *
  *   draft_probs [B, gamma, V] float32, finite (no NaN).
  *   tokens_out, parents_out [B, n_max] int32; n_nodes_out [B] int32.
- *   B >= 1; 1 <= gamma <= n_max <= 64; V >= 2; 0 <= k (<= 7 when fixed).
+ *   B >= 1; 1 <= gamma <= n_max <= 64; B * gamma <= 65535; V >= 2;
+ *   0 <= k (<= 7 when fixed).
  *   workspace >= cape_expand_workspace(B, gamma, V) bytes (no zero-fill needed).
  */
 int cape_expand(const float* draft_probs, int B, int gamma, int V, int k,
@@ -200,9 +201,12 @@ int tree_verify(const int32_t* target_argmax, const int32_t* cand_tokens,
  * only the accepted tokens' cache rows are kept; Sec. 4.2: a tree candidate
  * is accepted when its whole root path is).
  *
- * With L = seq_lens[b] and the accepted node's root path n_1, ..., n_a
- * (depths 1..a), every layer's K and V row L + n_d moves to row L + d - 1;
- * other rows are left as they are.  seq_lens_out[b] = L + a.
+ * With L = seq_lens[b] clamped into [0, L_cap - N] and the accepted node's
+ * root path n_1, ..., n_a (depths 1..a), every layer's K and V row L + n_d
+ * moves to row L + d - 1; other rows are left as they are.
+ * seq_lens_out[b] = L + a, with the same clamped L (so an out-of-range length
+ * that GLIDE_VALIDATE would reject still gives a length that matches the rows
+ * committed).
  *
  *   logits        [B, N + 1, V] float32: row 0 = the target's logits after
  *                 the prefix, row n + 1 = after tree node n.

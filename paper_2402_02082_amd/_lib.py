@@ -121,8 +121,22 @@ def _dev(t, name, dtype=None):
         _need(t.dtype == dtype, "%s must be %s" % (name, dtype))
 
 
+def _alloc_bytes(nbytes, device, stream=None):
+    """A byte buffer allocated on the stream that will use it.  torch's caching
+    allocator ties a block to the stream current at allocation and reuses it
+    for that stream's later work once freed; a buffer used on another stream
+    must be allocated there, or its memory could be handed to the current
+    stream's work while the kernels on `stream` still use it."""
+    if stream is None:
+        return torch.empty(nbytes, dtype=torch.uint8, device=device)
+    with torch.cuda.stream(stream):
+        return torch.empty(nbytes, dtype=torch.uint8, device=device)
+
+
 # Workspaces, kept per (device, stream) so that calls that may run
-# concurrently on different streams never share partial states.
+# concurrently on different streams never share partial states.  Each is
+# allocated on its stream (see _alloc_bytes), so a replaced one is only
+# reused after that stream's pending work.
 _ws_cache = {}
 
 
@@ -134,7 +148,7 @@ def attn_workspace(B, N, H, L_cap, max_splits, device, stream=None):
     key = (str(device), s.cuda_stream)
     ws = _ws_cache.get(key)
     if ws is None or ws.numel() < need:
-        ws = torch.empty(need, dtype=torch.uint8, device=device)
+        ws = _alloc_bytes(need, device, s)
         _ws_cache[key] = ws
     return ws
 
@@ -182,7 +196,7 @@ def cape_expand(draft_probs, k, n_max, tokens_out, parents_out, n_nodes_out, fix
         _need(tuple(t.shape) == shape, "%s must be %s" % (name, shape))
     need = load().cape_expand_workspace(B, gamma, V)
     if workspace is None:
-        workspace = torch.empty(max(need, 1), dtype=torch.uint8, device=draft_probs.device)
+        workspace = _alloc_bytes(max(need, 1), draft_probs.device, stream)
     status = load().cape_expand(
         _ptr(draft_probs), B, gamma, V, int(k), 1 if fixed else 0, int(n_max), _ptr(tokens_out),
         _ptr(parents_out), _ptr(n_nodes_out), _ptr(workspace),
@@ -300,7 +314,7 @@ def pack_rows_weights(w_t, out=None, stream=None):
     need = rows_weights_packed_bytes(K, N)
     _need(need > 0, "unsupported projection sizes")
     if out is None:
-        out = torch.empty(need // 2, dtype=torch.bfloat16, device=w_t.device)
+        out = _alloc_bytes(need, w_t.device, stream).view(torch.bfloat16)
     _dev(out, "out", torch.bfloat16)
     _need(out.numel() * 2 >= need, "out is smaller than the packed copy")
     status = load().glide_pack_rows_weights(_ptr(w_t), _ptr(out), K, N, _stream(stream, w_t.device))
@@ -325,10 +339,10 @@ def glide_rows_matmul_packed(a, w_packed, out, stream=None):
     return out
 
 
-def cross_block_workspace(B, Nq, d_D, H, L_cap, device):
+def cross_block_workspace(B, Nq, d_D, H, L_cap, device, stream=None):
     need = load().glide_cross_block_workspace(B, Nq, d_D, H, HEAD_DIM, L_cap)
     _need(need > 0, "unsupported cross-attention block sizes")
-    return torch.empty(need, dtype=torch.uint8, device=device)
+    return _alloc_bytes(need, device, stream)
 
 
 def glide_cross_block(hidden, wq_t, k_cache, v_cache, seq_lens, wo_t, out, scale=0.0,
@@ -349,7 +363,7 @@ def glide_cross_block(hidden, wq_t, k_cache, v_cache, seq_lens, wo_t, out, scale
     _need(tuple(out.shape) == (B, Nq, d_D), "out must be [B, Nq, d_D]")
     _need(seq_lens.shape == (B,), "seq_lens must be [B]")
     if workspace is None:
-        workspace = cross_block_workspace(B, Nq, d_D, H, L_cap, hidden.device)
+        workspace = cross_block_workspace(B, Nq, d_D, H, L_cap, hidden.device, stream)
     status = load().glide_cross_block(
         _ptr(hidden), _ptr(wq_t), _ptr(k_cache), _ptr(v_cache), _ptr(seq_lens), _ptr(wo_t),
         _ptr(out), B, Nq, d_D, H, D, L_cap, float(scale), _ptr(workspace),
@@ -377,7 +391,7 @@ def glide_cross_block_packed(hidden, wq_packed, k_cache, v_cache, seq_lens, wo_p
     _need(tuple(out.shape) == (B, Nq, d_D), "out must be [B, Nq, d_D]")
     _need(seq_lens.shape == (B,), "seq_lens must be [B]")
     if workspace is None:
-        workspace = cross_block_workspace(B, Nq, d_D, H, L_cap, hidden.device)
+        workspace = cross_block_workspace(B, Nq, d_D, H, L_cap, hidden.device, stream)
     status = load().glide_cross_block_packed(
         _ptr(hidden), _ptr(wq_packed), _ptr(k_cache), _ptr(v_cache), _ptr(seq_lens), _ptr(wo_packed),
         _ptr(out), B, Nq, d_D, H, D, L_cap, float(scale), _ptr(workspace),

@@ -96,6 +96,10 @@ bool rows_matmul_sizes_ok(int M, int K, int N) {
 
 size_t align256(size_t n) { return (n + 255) & ~(size_t)255; }
 
+// CaPE's part kernel runs one workgroup row per draft row: B * gamma is a
+// grid dimension (at most 65535).
+bool cape_rows_ok(int B, int gamma) { return (long)B * gamma <= 65535; }
+
 // Workspace of the cross-attention block: projected queries, concatenated
 // heads (both bf16 [B, Nq, H, D]) and the attention's split partials.
 struct CrossPlan {
@@ -168,7 +172,7 @@ int glide_tree_attn(const void* q, const void* k_cache, const void* v_cache, con
 }
 
 size_t cape_expand_workspace(int B, int gamma, int V) {
-  if (B < 1 || gamma < 1 || gamma > glide::kMaxNodes || V < 2) return 0;
+  if (B < 1 || gamma < 1 || gamma > glide::kMaxNodes || V < 2 || !cape_rows_ok(B, gamma)) return 0;
   return glide::cape_workspace_bytes(B, gamma, V);
 }
 
@@ -177,6 +181,7 @@ int cape_expand(const float* draft_probs, int B, int gamma, int V, int k, int fi
                 size_t ws_bytes, hipStream_t stream) {
   if (!draft_probs || !tokens_out || !parents_out || !n_nodes_out || !workspace) return GLIDE_EINVAL;
   if (B < 1 || gamma < 1 || n_max < gamma || n_max > glide::kMaxNodes || V < 2) return GLIDE_EINVAL;
+  if (!cape_rows_ok(B, gamma)) return GLIDE_EINVAL;
   if (k < 0 || (fixed && k > GLIDE_CAPE_MAX_K)) return GLIDE_EINVAL;
   if ((double)B * gamma * V > 9.0e18) return GLIDE_EINVAL;
   if (ws_bytes < glide::cape_workspace_bytes(B, gamma, V)) return GLIDE_EINVAL;

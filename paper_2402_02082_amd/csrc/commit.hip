@@ -83,10 +83,14 @@ __global__ __launch_bounds__(64 * kWaves) void verify_commit_kernel(CommitArgs a
   __shared__ int node_of[kWaves][64];
   if (on_path) node_of[wave][rank] = lane;
 
+  // The prefix length the rows are moved at: clamped into [0, L_cap - N]
+  // like every other reader of the lengths, and the committed length is
+  // that same clamped value plus the accepted count.
+  const int L = min(max(args.seq_lens[b], 0), args.L_cap - N);
   if (blockIdx.x == 0 && wave == 0) {
     if (lane == 0) {
       args.accept_len[b] = a;
-      args.seq_lens_out[b] = args.seq_lens[b] + a;
+      args.seq_lens_out[b] = L + a;
       if (args.last_node) args.last_node[b] = last;
       if (args.bonus) args.bonus[b] = ta[last + 1];
     }
@@ -102,7 +106,6 @@ __global__ __launch_bounds__(64 * kWaves) void verify_commit_kernel(CommitArgs a
   const int lanes_per_row = R / 16;
   const int rows_per_load = 64 / lanes_per_row;
   const int chunk = lane % lanes_per_row, q = lane / lanes_per_row;
-  const int L = min(max(args.seq_lens[b], 0), args.L_cap - N);
   const int s_begin = blockIdx.x * slabs_per_wg;
   const int s_end = min(args.layers * H, s_begin + slabs_per_wg);
   const int w = __builtin_amdgcn_readfirstlane(wave);

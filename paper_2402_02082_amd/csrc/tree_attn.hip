@@ -125,8 +125,6 @@ __device__ __forceinline__ uint32_t pack_bf16x2(float lo, float hi) {
   return __builtin_bit_cast(uint32_t, __builtin_convertvector(f, bf16x2_t));
 }
 
-__device__ __forceinline__ float bf16_lo(uint32_t w) { return __uint_as_float(w << 16); }
-__device__ __forceinline__ float bf16_hi(uint32_t w) { return __uint_as_float(w & 0xFFFF0000u); }
 
 // Element types ------------------------------------------------------------
 
@@ -185,11 +183,15 @@ __device__ __forceinline__ void load_q<F32Path>(F32Path::QFrag& f, const float* 
 // no swizzle, raw (unstrided) addressing.
 constexpr int kBufferDesc3 = 0x00020000;
 
+// The range is a 32-bit unsigned byte count: at most 2^22 rows of 512 bytes
+// (float32), i.e. 2^31, which the descriptor field holds but an int does not,
+// so it is formed unsigned and passed on as the same bits.
 __device__ __forceinline__ __amdgpu_buffer_rsrc_t step_rsrc(const char* slab, int j0, int k_end,
                                                             int row_bytes) {
-  const int rows = max(k_end - j0, 0);
+  const uint32_t rows = (uint32_t)max(k_end - j0, 0);
+  const uint32_t range = rows * (uint32_t)row_bytes;
   return __builtin_amdgcn_make_buffer_rsrc(const_cast<char*>(slab) + (size_t)j0 * row_bytes,
-                                           (short)0, rows * row_bytes, kBufferDesc3);
+                                           (short)0, __builtin_bit_cast(int, range), kBufferDesc3);
 }
 
 // Cache policy of the K/V loads: kStream marks them non-temporal (each row is

@@ -92,6 +92,8 @@ def _cape(lib, **kw):
     dict(p=None), dict(t=None), dict(par=None), dict(n=None), dict(ws=None), dict(B=0),
     dict(gamma=0), dict(gamma=17), dict(n_max=65, gamma=5), dict(V=1), dict(k=-1),
     dict(fixed=1, k=8), dict(ws_bytes=8),
+    # B * gamma draft rows are a grid dimension: at most 65535
+    dict(B=1025, gamma=64, n_max=64, ws_bytes=1 << 40), dict(B=65535, gamma=2, ws_bytes=1 << 40),
 ])
 def test_cape_rejects(lib, bad):
     assert _cape(lib, **bad) == glide.GLIDE_EINVAL
@@ -104,6 +106,19 @@ def test_cape_workspace(lib):
     assert lib.cape_expand_workspace(0, 5, 100) == 0
     assert lib.cape_expand_workspace(1, 65, 100) == 0
     assert lib.cape_expand_workspace(1, 5, 1) == 0
+    assert lib.cape_expand_workspace(13107, 5, 100) > 0      # 65535 rows
+    assert lib.cape_expand_workspace(13108, 5, 100) == 0     # 65540 rows
+    assert lib.cape_expand_workspace(1025, 64, 100) == 0
+
+
+def test_tree_attn_size_limit(lib):
+    """The largest accepted cache, 2^22 rows, in float32 is 2^31 bytes per
+    (sequence, head) slab: accepted (the kernels form that byte range
+    unsigned), one row more is rejected; the same in bfloat16."""
+    assert lib.glide_tree_attn_workspace(1, 1, 1, 128, 1 << 22, 2) > 0
+    assert lib.glide_tree_attn_workspace(1, 1, 1, 128, (1 << 22) + 1, 2) == 0
+    for dtype in (0, 1):
+        assert _attn(lib, L_cap=(1 << 22) + 1, dtype=dtype, B=1, H=1, N=1) == glide.GLIDE_EINVAL
 
 
 @pytest.mark.parametrize("args", [

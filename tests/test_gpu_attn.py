@@ -228,3 +228,31 @@ def test_peaked_scores(N, kind, dtype):
     else:
         err = float(np.abs(got - ref).max())
         assert err <= 24 * F32_TOL, err
+
+
+@pytest.mark.parametrize("splits", [1, 0])
+def test_largest_float32_cache(splits):
+    """L_cap = 2^22 rows in float32, the largest accepted: a (sequence, head)
+    slab of exactly 2^31 bytes, which one split reads through a single byte
+    range.  Zero queries give every key weight 2^-22 exactly; the values are
+    1 except the node's own row (the last one), which is 2^22 + 1, so the
+    exact output is 2^23 / 2^22 = 2 -- and any row left unread (a truncated
+    range) would pull it towards 1.  Every partial sum is an integer below
+    2^24, so float32 holds them exactly."""
+    require_gpu()
+    dev = torch.device("cuda")
+    L_cap = 1 << 22
+    say("tree_attn largest float32 cache", dict(L_cap=L_cap, splits=splits))
+    q = torch.zeros((1, 1, 1, D), dtype=torch.float32, device=dev)
+    k = torch.zeros((1, 1, L_cap, D), dtype=torch.float32, device=dev)
+    v = torch.ones((1, 1, L_cap, D), dtype=torch.float32, device=dev)
+    v[0, 0, L_cap - 1] = float(L_cap + 1)
+    lens = torch.tensor([L_cap - 1], dtype=torch.int32, device=dev)
+    parents = torch.tensor([[-1]], dtype=torch.int32, device=dev)
+    out = torch.full_like(q, float("nan"))
+    glide.glide_tree_attn(q, k, v, lens, parents, out, max_splits=splits)
+    torch.cuda.synchronize()
+    got = out.cpu().numpy()
+    del q, k, v
+    torch.cuda.empty_cache()
+    assert np.all(got == 2.0), got.ravel()[:4]

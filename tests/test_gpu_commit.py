@@ -148,6 +148,39 @@ def test_seq_lens_validation(monkeypatch):
     assert e.value.status == glide.GLIDE_ERANGE
 
 
+def test_out_of_range_lengths_are_clamped():
+    """Without GLIDE_VALIDATE, lengths past L_cap - N (and negative ones) are
+    clamped into [0, L_cap - N]; the rows move at the clamped length and the
+    committed length is that clamped length plus the accepted count.  The
+    expected values are the oracle's at the clamped lengths."""
+    require_gpu()
+    B, N = 3, 8
+    logits, cand, parents, _ = make_case(12, B, N, none_frac=0.0)
+    L_cap = 20
+    raw = np.array([L_cap + 5, -4, L_cap - N + 1], dtype=np.int32)
+    clamped = np.clip(raw, 0, L_cap - N).astype(np.int32)
+    for dtype in (torch.bfloat16, torch.float32):
+        ks, vs = _caches(12, B, 2, L_cap, 2, dtype)
+        k_in = [_bits(k) for k in ks]
+        v_in = [_bits(v) for v in vs]
+        dev = torch.device("cuda")
+        lens_out = torch.full((B,), -7, dtype=torch.int32, device=dev)
+        acc = torch.empty((B,), dtype=torch.int32, device=dev)
+        ta = torch.empty((B, N + 1), dtype=torch.int32, device=dev)
+        say("verify_commit", "clamped lengths", dtype, raw.tolist())
+        glide.glide_verify_commit(torch.from_numpy(logits).to(dev), torch.from_numpy(cand).to(dev),
+                                  torch.from_numpy(parents).to(dev), ks, vs,
+                                  torch.from_numpy(raw).to(dev), lens_out, ta, acc)
+        torch.cuda.synchronize()
+        want = OCm.verify_commit(logits, cand, parents, clamped, k_in, v_in)
+        assert want["accept_len"].max() > 0
+        assert np.array_equal(acc.cpu().numpy(), want["accept_len"])
+        assert np.array_equal(lens_out.cpu().numpy(), want["seq_lens_out"])
+        for l in range(len(ks)):
+            assert np.array_equal(_bits(ks[l]), want["k_out"][l]), ("k", l)
+            assert np.array_equal(_bits(vs[l]), want["v_out"][l]), ("v", l)
+
+
 @pytest.mark.parametrize("cfg,layers", [(2, None), (3, [0, 39]), (4, [59])])
 def test_workload(cfg, layers):
     """A workload's CaPE tree (built on the GPU), its planted logits and its

@@ -8,8 +8,9 @@ For every workload:
   and the planted accept length is recovered;
 * verification attention of the first and last layer with the tree the GPU
   built, and (where the workload has one) the GliDe cross-attention on the
-  last layer's cache -- sampled (sequence, head, node) outputs against the
-  float64 oracle, max-abs error <= 1e-2.
+  last layer's cache -- every sequence, heads {0, H/2, H-1} and sampled nodes
+  (every chain node and a middle node of every depth) against the float64
+  oracle, max-abs error <= 1e-2.
 """
 
 import numpy as np
@@ -39,8 +40,20 @@ def _gpu_tree(wl, probs, k):
     return t, p, n
 
 
-def _sample_nodes(N, depth):
-    return sorted({0, depth - 1, min(depth, N - 1), N // 2, N - 1, 1 % N})
+def _sample_nodes(parents_b, N, depth):
+    """Nodes compared against the oracle: every chain node, a middle node of
+    every depth (the middle leaf of that depth's expansion set when it has
+    one), the middle and the last node."""
+    d = np.zeros(N, dtype=np.int64)
+    for n in range(N):
+        p = int(parents_b[n])
+        d[n] = 1 + (d[p] if p >= 0 else 0)
+    pick = set(range(min(depth, N))) | {N // 2, N - 1}
+    for level in range(1, int(d.max()) + 1):
+        at = [n for n in range(N) if d[n] == level and n >= depth]
+        if at:
+            pick.add(at[len(at) // 2])
+    return sorted(pick)
 
 
 @pytest.mark.parametrize("cfg", [1, 2, 3, 4, 5])
@@ -92,9 +105,8 @@ def test_attention(cfg):
     else:
         par_or = np.tile(np.arange(-1, wl.nodes - 1, dtype=np.int32), (wl.batch, 1))
         par_gpu = torch.from_numpy(par_or).to(dev)
-    seqs = sorted({0, wl.batch - 1})
+    seqs = range(wl.batch)
     heads = sorted({0, wl.heads // 2, wl.heads - 1})
-    nodes = _sample_nodes(wl.nodes, wl.depth)
     for layer in sorted({0, wl.layers - 1}):
         say("attention", wl.name, "layer", layer)
         q, k, v = W.attention_layer(wl, SEED, layer, torch.bfloat16, dev)
@@ -102,6 +114,7 @@ def test_attention(cfg):
         glide.glide_tree_attn(q, k, v, lens, par_gpu, out)
         torch.cuda.synchronize()
         for b in seqs:
+            nodes = _sample_nodes(par_or[b], wl.nodes, wl.depth)
             for h in heads:
                 L = int(lens_np[b])
                 rows = L + wl.nodes
@@ -150,8 +163,8 @@ def test_attention_f32(cfg):
     out = torch.full_like(q, float("nan"))
     glide.glide_tree_attn(q, k, v, lens, par_gpu, out)
     torch.cuda.synchronize()
-    nodes = _sample_nodes(wl.nodes, wl.depth)
-    for b in sorted({0, wl.batch - 1}):
+    for b in range(wl.batch):
+        nodes = _sample_nodes(par_or[b], wl.nodes, wl.depth)
         for h in sorted({0, wl.heads // 2, wl.heads - 1}):
             L = int(lens_np[b])
             rows = L + wl.nodes
