@@ -163,3 +163,37 @@ def test_two_streams_own_workspaces():
     got = (st["out"], st["xb_out"], other["out"], other["xb_out"])
     for a, b in zip(got, want):
         assert torch.equal(a.view(torch.int16), b.view(torch.int16))
+
+
+def test_explicit_stream_argument():
+    """Calls given stream= a stream that is not the current one: the binding
+    allocates their temporary workspaces (CaPE's, the cross block's, the
+    attention's cached one and the packed weights) on that stream, so memory
+    the current stream then allocates and scribbles on is never one of them
+    while the calls run.  Results match the calls made on the current stream."""
+    require_gpu()
+    say("explicit stream argument")
+    st = _inputs()
+    _calls(st)
+    torch.cuda.synchronize()
+    want = {k: st[k].clone() for k in ("tok", "par", "nn", "out", "xb_out")}
+    for k in want:
+        st[k].fill_(-5 if st[k].dtype == torch.int32 else float("nan"))
+    s = torch.cuda.Stream()
+    s.wait_stream(torch.cuda.current_stream())
+    for _ in range(3):
+        glide.cape_expand(st["probs"], 7, st["tok"].shape[1], st["tok"], st["par"], st["nn"], stream=s)
+        glide.glide_tree_attn(st["q"], st["kc"], st["vc"], st["lens"], st["par"], st["out"], stream=s)
+        wq_p = glide.pack_rows_weights(st["wq"], stream=s)
+        glide.glide_cross_block_packed(st["hidden"], wq_p, st["kc"], st["vc"], st["lens"], st["wo_p"],
+                                       st["xb_out"], stream=s)
+        del wq_p
+        # the current stream allocates and overwrites freed memory meanwhile
+        junk = [torch.full((1 << 20,), float("nan"), device="cuda") for _ in range(8)]
+        del junk
+    torch.cuda.synchronize()
+    for k, w in want.items():
+        a = st[k]
+        same = torch.equal(a.view(torch.int16), w.view(torch.int16)) if a.dtype == torch.bfloat16 \
+            else torch.equal(a, w)
+        assert same, k
