@@ -206,7 +206,9 @@ int tree_verify(const int32_t* target_argmax, const int32_t* cand_tokens,
  * moves to row L + d - 1; other rows are left as they are.
  * seq_lens_out[b] = L + a, with the same clamped L (so an out-of-range length
  * that GLIDE_VALIDATE would reject still gives a length that matches the rows
- * committed).
+ * committed).  With layers == 0 there is no cache: L_cap is not used,
+ * seq_lens[b] is taken as given (no clamp, no validation) and
+ * seq_lens_out[b] = seq_lens[b] + a.
  *
  *   logits        [B, N + 1, V] float32: row 0 = the target's logits after
  *                 the prefix, row n + 1 = after tree node n.
@@ -223,8 +225,8 @@ int tree_verify(const int32_t* target_argmax, const int32_t* cand_tokens,
  *                 (accepted node at depth d + 1 in slot d, -1 after) int32
  *                 out, nullable.
  *   B <= 65535; 1 <= N <= 64; B * N * H < 2^31; D == 128;
- *   N <= L_cap <= 4194304; seq_lens[b] + N <= L_cap (clamped into range
- *   unless GLIDE_VALIDATE=1).
+ *   N <= L_cap <= 4194304; seq_lens[b] + N <= L_cap when layers > 0
+ *   (clamped into range unless GLIDE_VALIDATE=1).
  * Two launches (the argmax, then the acceptance and copy); no workspace.
  */
 int glide_verify_commit(const float* logits, int V, const int32_t* cand_tokens,

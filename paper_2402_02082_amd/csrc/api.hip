@@ -235,9 +235,11 @@ int glide_verify_commit(const float* logits, int V, const int32_t* cand_tokens, 
   if (validate_enabled()) {
     int status = GLIDE_OK;
     std::vector<int32_t> lens, par;
-    if (!fetch_ints(seq_lens, (size_t)B, lens, stream, &status)) return status;
-    for (int b = 0; b < B; ++b)
-      if (lens[b] < 0 || lens[b] > L_cap - N) return GLIDE_ERANGE;
+    if (layers > 0) {  // the lengths must fit the caches they index
+      if (!fetch_ints(seq_lens, (size_t)B, lens, stream, &status)) return status;
+      for (int b = 0; b < B; ++b)
+        if (lens[b] < 0 || lens[b] > L_cap - N) return GLIDE_ERANGE;
+    }
     if (!fetch_ints(parents, (size_t)B * N, par, stream, &status)) return status;
     if (!parents_ok(par, B, N)) return GLIDE_ERANGE;
   }

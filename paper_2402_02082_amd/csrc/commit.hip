@@ -83,10 +83,13 @@ __global__ __launch_bounds__(64 * kWaves) void verify_commit_kernel(CommitArgs a
   __shared__ int node_of[kWaves][64];
   if (on_path) node_of[wave][rank] = lane;
 
-  // The prefix length the rows are moved at: clamped into [0, L_cap - N]
-  // like every other reader of the lengths, and the committed length is
-  // that same clamped value plus the accepted count.
-  const int L = min(max(args.seq_lens[b], 0), args.L_cap - N);
+  // The prefix length the rows are moved at: with caches to commit, clamped
+  // into [0, L_cap - N] like every other reader of the lengths, and the
+  // committed length is that same clamped value plus the accepted count;
+  // with no caches (layers == 0) there is no cache bound and the length is
+  // taken as given.
+  const int raw_len = args.seq_lens[b];
+  const int L = args.layers > 0 ? min(max(raw_len, 0), args.L_cap - N) : raw_len;
   if (blockIdx.x == 0 && wave == 0) {
     if (lane == 0) {
       args.accept_len[b] = a;
