@@ -65,6 +65,8 @@ extern "C" {
 #define GLIDE_EINVAL  1   /* bad pointer, size, dtype or option */
 #define GLIDE_ERANGE  2   /* device data out of range (GLIDE_VALIDATE=1 only) */
 #define GLIDE_EHIP    3   /* a HIP call or kernel launch failed */
+#define GLIDE_ESCRATCH 4  /* sizes need more than glide_tree_attn_noalloc's
+                             fixed scratch holds */
 
 /* Element types of q / k_cache / v_cache / out. */
 #define GLIDE_BF16    0   /* bfloat16 in and out, float32 accumulation */
@@ -130,6 +132,30 @@ int glide_tree_attn(const void* q, const void* k_cache, const void* v_cache,
                     void* out, int B, int N, int H, int D, int L_cap,
                     int dtype, float scale, int max_splits,
                     void* workspace, size_t ws_bytes, hipStream_t stream);
+
+/*
+ * glide_tree_attn_noalloc -- glide_tree_attn for callers that cannot
+ * allocate device memory (code under HIP graph capture, tight serving loops,
+ * harnesses that forbid allocation).  Same arguments, same kernels and the
+ * same results as glide_tree_attn with max_splits alike, but no workspace
+ * argument: the split partial states live in a fixed scratch array of
+ * glide_tree_attn_noalloc_max_workspace() bytes (16 MiB) that the library
+ * holds on every GPU it runs on until the process ends.  The call allocates
+ * nothing and records no memset (the partials are written before they are
+ * read).  Sizes whose split plan needs more than the scratch holds
+ * (glide_tree_attn_workspace(...) > the maximum) return GLIDE_ESCRATCH
+ * before any HIP call; sizes that need no workspace never touch it.
+ * The first call on a device, with that device current, looks up the
+ * scratch array's device address (hipGetSymbolAddress).
+ * Every call on one GPU shares that GPU's scratch: calls that can overlap on
+ * one GPU (other streams, other host threads) race and must not be issued.
+ */
+size_t glide_tree_attn_noalloc_max_workspace(void);
+int glide_tree_attn_noalloc(const void* q, const void* k_cache, const void* v_cache,
+                            const int32_t* seq_lens, const int32_t* tree_parents,
+                            void* out, int B, int N, int H, int D, int L_cap,
+                            int dtype, float scale, int max_splits,
+                            hipStream_t stream);
 
 /* Workspace bytes cape_expand needs (the best candidates of every 4096-token
  * part of every draft row); 0 for invalid sizes (as cape_expand rejects). */

@@ -4,6 +4,8 @@ Thin Python face of libglide.so (HIP kernels behind a C ABI, declared in
 include/glide.h).  Functions carry the C names:
 
     glide_tree_attn   tree-masked / cross attention against a KV cache
+    glide_tree_attn_noalloc  the same with the split partials in the
+                      library's fixed scratch (for callers that cannot allocate)
     cape_expand       confidence-aware proposal expansion into a tree
     glide_argmax_rows the target's greedy token per logits row
     tree_verify       greedy longest-accepted-path selection
@@ -22,11 +24,13 @@ PyTorch only provides device memory and streams.
 """
 
 from ._lib import (  # noqa: F401
-    CAPE_MAX_K, GLIDE_BF16, GLIDE_EHIP, GLIDE_EINVAL, GLIDE_ERANGE, GLIDE_F32, GLIDE_OK,
+    CAPE_MAX_K, GLIDE_BF16, GLIDE_EHIP, GLIDE_EINVAL, GLIDE_ERANGE, GLIDE_ESCRATCH, GLIDE_F32,
+    GLIDE_OK,
     HEAD_DIM, MAX_NODES, MAX_SPLITS, GlideError, attn_workspace, cape_expand,
     cross_block_workspace, glide_argmax_rows, glide_block_attn, glide_cross_block,
     glide_cross_block_packed, glide_rows_matmul, glide_rows_matmul_packed, pack_rows_weights,
     rows_weights_packed_bytes,
-    glide_expected_speedup, glide_tree_attn, glide_verify_commit, load, spec_sample_verify,
+    glide_expected_speedup, glide_tree_attn, glide_tree_attn_noalloc, glide_verify_commit, load,
+    spec_sample_verify,
     tree_verify,
 )

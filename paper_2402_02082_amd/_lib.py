@@ -14,7 +14,7 @@ import torch
 _PKG = os.path.dirname(os.path.abspath(__file__))
 LIB_PATH = os.path.join(_PKG, "libglide.so")
 
-GLIDE_OK, GLIDE_EINVAL, GLIDE_ERANGE, GLIDE_EHIP = 0, 1, 2, 3
+GLIDE_OK, GLIDE_EINVAL, GLIDE_ERANGE, GLIDE_EHIP, GLIDE_ESCRATCH = 0, 1, 2, 3, 4
 GLIDE_BF16, GLIDE_F32 = 0, 1
 MAX_NODES, MAX_SPLITS, HEAD_DIM, CAPE_MAX_K = 64, 64, 128, 7
 
@@ -48,6 +48,10 @@ def load():
     lib.glide_tree_attn_workspace.argtypes = [I, I, I, I, I, I]
     lib.glide_tree_attn.restype = I
     lib.glide_tree_attn.argtypes = [P, P, P, P, P, P, I, I, I, I, I, I, F, I, P, Z, P]
+    lib.glide_tree_attn_noalloc_max_workspace.restype = Z
+    lib.glide_tree_attn_noalloc_max_workspace.argtypes = []
+    lib.glide_tree_attn_noalloc.restype = I
+    lib.glide_tree_attn_noalloc.argtypes = [P, P, P, P, P, P, I, I, I, I, I, I, F, I, P]
     lib.cape_expand_workspace.restype = Z
     lib.cape_expand_workspace.argtypes = [I, I, I]
     lib.cape_expand.restype = I
@@ -84,7 +88,8 @@ def load():
 
 
 EXPORTED = ["glide_strerror", "glide_last_hip_error", "glide_tree_attn_workspace",
-            "glide_tree_attn", "cape_expand_workspace", "cape_expand",
+            "glide_tree_attn", "glide_tree_attn_noalloc_max_workspace", "glide_tree_attn_noalloc",
+            "cape_expand_workspace", "cape_expand",
             "glide_argmax_rows", "tree_verify", "glide_verify_commit", "glide_rows_matmul",
             "glide_rows_weights_packed_bytes", "glide_pack_rows_weights", "glide_rows_matmul_packed",
             "glide_cross_block_workspace", "glide_cross_block", "glide_cross_block_packed",
@@ -181,6 +186,33 @@ def glide_tree_attn(q, k_cache, v_cache, seq_lens, tree_parents, out, scale=0.0,
         B, N, H, D, L_cap, dtype, float(scale), int(max_splits), _ptr(workspace), ws_bytes,
         _stream(stream, q.device))
     _check("glide_tree_attn", status)
+    return out
+
+
+def glide_tree_attn_noalloc(q, k_cache, v_cache, seq_lens, tree_parents, out, scale=0.0,
+                            max_splits=0, stream=None):
+    """glide_tree_attn without a workspace: the split partials use the
+    library's fixed per-device scratch (no allocation anywhere on this path).
+    Calls that overlap on one GPU race; see include/glide.h."""
+    _dev(q, "q")
+    _need(q.dtype in (torch.bfloat16, torch.float32), "q must be bfloat16 or float32")
+    for name, t in (("k_cache", k_cache), ("v_cache", v_cache), ("out", out)):
+        _dev(t, name, q.dtype)
+    _dev(seq_lens, "seq_lens", torch.int32)
+    B, N, H, D = q.shape
+    _need(k_cache.dim() == 4 and k_cache.shape[:2] == (B, H) and k_cache.shape[3] == D,
+          "k_cache must be [B, H, L_cap, D]")
+    _need(v_cache.shape == k_cache.shape, "v_cache must match k_cache")
+    _need(out.shape == q.shape, "out must match q")
+    _need(seq_lens.shape == (B,), "seq_lens must be [B]")
+    if tree_parents is not None:
+        _dev(tree_parents, "tree_parents", torch.int32)
+        _need(tree_parents.shape == (B, N), "tree_parents must be [B, N]")
+    status = load().glide_tree_attn_noalloc(
+        _ptr(q), _ptr(k_cache), _ptr(v_cache), _ptr(seq_lens), _ptr(tree_parents), _ptr(out),
+        B, N, H, D, k_cache.shape[2], GLIDE_BF16 if q.dtype == torch.bfloat16 else GLIDE_F32,
+        float(scale), int(max_splits), _stream(stream, q.device))
+    _check("glide_tree_attn_noalloc", status)
     return out
 
 

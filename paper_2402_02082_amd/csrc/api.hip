@@ -6,10 +6,15 @@
 #include <stdlib.h>
 #include <string.h>
 
+#include <mutex>
 #include <vector>
 
 #include "glide.h"
 #include "internal.h"
+
+// Fixed scratch of glide_tree_attn_noalloc (see scratch_of_current_device).
+static constexpr size_t kNoAllocScratchBytes = (size_t)16 << 20;
+static __device__ __align__(256) char scratch[kNoAllocScratchBytes];
 
 namespace {
 
@@ -119,32 +124,45 @@ bool cross_block_plan(int B, int Nq, int d_D, int H, int D, int L_cap, CrossPlan
   return true;
 }
 
-}  // namespace
+// ---------------------------------------------------------------------------
+// Fixed scratch of glide_tree_attn_noalloc, for callers that cannot allocate:
+// a file-scope device array that every GPU the library runs on holds until
+// the process ends.  In host code `scratch` names a host-side stand-in, not
+// the device memory, so its device address is looked up once per device
+// (with that device current) and only that address is used from then on.
+// ---------------------------------------------------------------------------
+constexpr int kMaxDevices = 64;
 
-extern "C" {
 
-const char* glide_strerror(int status) {
-  switch (status) {
-    case GLIDE_OK: return "ok";
-    case GLIDE_EINVAL: return "invalid argument";
-    case GLIDE_ERANGE: return "device data out of range";
-    case GLIDE_EHIP: return "HIP error";
-    default: return "unknown status";
+std::mutex g_scratch_mu;
+void* g_scratch_ptr[kMaxDevices];
+
+int scratch_of_current_device(void** ptr) {
+  int dev = -1;
+  hipError_t e = hipGetDevice(&dev);
+  if (e != hipSuccess) return hip_status(e);
+  if (dev < 0 || dev >= kMaxDevices) return GLIDE_EINVAL;
+  std::lock_guard<std::mutex> lock(g_scratch_mu);
+  if (!g_scratch_ptr[dev]) {
+    void* p = nullptr;
+    e = hipGetSymbolAddress(&p, HIP_SYMBOL(scratch));
+    if (e != hipSuccess) return hip_status(e);
+    if (!p) return hip_status(hipErrorInvalidSymbol);
+    g_scratch_ptr[dev] = p;
   }
+  *ptr = g_scratch_ptr[dev];
+  return GLIDE_OK;
 }
 
-int glide_last_hip_error(void) { return g_last_hip_error; }
 
-size_t glide_tree_attn_workspace(int B, int N, int H, int D, int L_cap, int max_splits) {
-  if (!tree_attn_sizes_ok(B, N, H, D, L_cap, false)) return 0;
-  if (max_splits < 0 || max_splits > glide::kMaxSplits) return 0;
-  return glide::plan_tree_attn(B, N, H, L_cap, max_splits).ws_bytes;
-}
-
-int glide_tree_attn(const void* q, const void* k_cache, const void* v_cache, const int32_t* seq_lens,
-                    const int32_t* tree_parents, void* out, int B, int N, int H, int D, int L_cap,
-                    int dtype, float scale, int max_splits, void* workspace, size_t ws_bytes,
-                    hipStream_t stream) {
+// Shared body of glide_tree_attn and glide_tree_attn_noalloc.  With
+// `scratch` set, the split partials go to the per-device scratch array that
+// it resolves (after every host-side check) instead of the caller's
+// workspace, and plans that need more than that array holds are refused.
+int tree_attn_call(const void* q, const void* k_cache, const void* v_cache, const int32_t* seq_lens,
+                   const int32_t* tree_parents, void* out, int B, int N, int H, int D, int L_cap,
+                   int dtype, float scale, int max_splits, void* workspace, size_t ws_bytes,
+                   int (*scratch)(void** ptr), hipStream_t stream) {
   const bool tree = tree_parents != nullptr;
   if (!q || !k_cache || !v_cache || !seq_lens || !out) return GLIDE_EINVAL;
   if (dtype != GLIDE_BF16 && dtype != GLIDE_F32) return GLIDE_EINVAL;
@@ -152,6 +170,14 @@ int glide_tree_attn(const void* q, const void* k_cache, const void* v_cache, con
   if (max_splits < 0 || max_splits > glide::kMaxSplits) return GLIDE_EINVAL;
   if (!isfinite(scale)) return GLIDE_EINVAL;
   const glide::AttnPlan plan = glide::plan_tree_attn(B, N, H, L_cap, max_splits);
+  if (scratch) {
+    if (plan.ws_bytes > kNoAllocScratchBytes) return GLIDE_ESCRATCH;
+    if (plan.ws_bytes > 0) {
+      const int st = scratch(&workspace);
+      if (st != GLIDE_OK) return st;
+      ws_bytes = kNoAllocScratchBytes;
+    }
+  }
   if (plan.ws_bytes > 0 && (!workspace || ws_bytes < plan.ws_bytes)) return GLIDE_EINVAL;
 
   if (validate_enabled()) {
@@ -169,6 +195,48 @@ int glide_tree_attn(const void* q, const void* k_cache, const void* v_cache, con
   const glide::AttnArgs a = attn_args(q, k_cache, v_cache, seq_lens, tree_parents, out, B, N, H, D,
                                       L_cap, scale, plan, workspace);
   return hip_status(glide::launch_tree_attn(a, dtype == GLIDE_BF16, stream));
+}
+
+
+}  // namespace
+
+extern "C" {
+
+const char* glide_strerror(int status) {
+  switch (status) {
+    case GLIDE_OK: return "ok";
+    case GLIDE_EINVAL: return "invalid argument";
+    case GLIDE_ERANGE: return "device data out of range";
+    case GLIDE_EHIP: return "HIP error";
+    case GLIDE_ESCRATCH: return "sizes need more than the fixed scratch of the no-allocation call";
+    default: return "unknown status";
+  }
+}
+
+int glide_last_hip_error(void) { return g_last_hip_error; }
+
+size_t glide_tree_attn_workspace(int B, int N, int H, int D, int L_cap, int max_splits) {
+  if (!tree_attn_sizes_ok(B, N, H, D, L_cap, false)) return 0;
+  if (max_splits < 0 || max_splits > glide::kMaxSplits) return 0;
+  return glide::plan_tree_attn(B, N, H, L_cap, max_splits).ws_bytes;
+}
+
+int glide_tree_attn(const void* q, const void* k_cache, const void* v_cache, const int32_t* seq_lens,
+                    const int32_t* tree_parents, void* out, int B, int N, int H, int D, int L_cap,
+                    int dtype, float scale, int max_splits, void* workspace, size_t ws_bytes,
+                    hipStream_t stream) {
+  return tree_attn_call(q, k_cache, v_cache, seq_lens, tree_parents, out, B, N, H, D, L_cap, dtype, scale,
+                        max_splits, workspace, ws_bytes, nullptr, stream);
+}
+
+size_t glide_tree_attn_noalloc_max_workspace(void) { return kNoAllocScratchBytes; }
+
+int glide_tree_attn_noalloc(const void* q, const void* k_cache, const void* v_cache,
+                            const int32_t* seq_lens, const int32_t* tree_parents, void* out, int B, int N,
+                            int H, int D, int L_cap, int dtype, float scale, int max_splits,
+                            hipStream_t stream) {
+  return tree_attn_call(q, k_cache, v_cache, seq_lens, tree_parents, out, B, N, H, D, L_cap, dtype, scale,
+                        max_splits, nullptr, 0, &scratch_of_current_device, stream);
 }
 
 size_t cape_expand_workspace(int B, int gamma, int V) {

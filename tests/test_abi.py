@@ -65,6 +65,37 @@ def test_tree_attn_rejects(lib, bad):
     assert _attn(lib, **bad) == glide.GLIDE_EINVAL
 
 
+def _noalloc(lib, **kw):
+    a = dict(q=FAKE, k=FAKE, v=FAKE, lens=FAKE, parents=FAKE, out=FAKE, B=1, N=16, H=32, D=128,
+             L_cap=2064, dtype=0, scale=0.0, splits=0)
+    a.update(kw)
+    return lib.glide_tree_attn_noalloc(a["q"], a["k"], a["v"], a["lens"], a["parents"], a["out"],
+                                       a["B"], a["N"], a["H"], a["D"], a["L_cap"], a["dtype"],
+                                       a["scale"], a["splits"], None)
+
+
+@pytest.mark.parametrize("bad", [
+    dict(q=None), dict(out=None), dict(N=65), dict(D=64), dict(dtype=2), dict(splits=65),
+    dict(scale=float("nan")), dict(L_cap=(1 << 22) + 1),
+])
+def test_tree_attn_noalloc_rejects(lib, bad):
+    assert _noalloc(lib, **bad) == glide.GLIDE_EINVAL
+
+
+def test_tree_attn_noalloc_scratch_limit(lib):
+    """Plans needing more workspace than the fixed scratch are refused with
+    their own status before any HIP call."""
+    cap = lib.glide_tree_attn_noalloc_max_workspace()
+    assert cap == 16 << 20
+    assert lib.glide_tree_attn_workspace(8, 64, 52, 128, 8256, 64) > cap
+    assert _noalloc(lib, B=8, N=64, H=52, L_cap=8256, splits=64) == glide.GLIDE_ESCRATCH
+    assert lib.glide_strerror(glide.GLIDE_ESCRATCH).startswith(b"sizes need more")
+    # the workloads' automatic plans fit
+    for B, N, H, L_cap in ((1, 16, 32, 2064), (4, 32, 40, 4128), (8, 64, 52, 8256),
+                           (16, 64, 32, 32832), (16, 5, 32, 32832)):
+        assert lib.glide_tree_attn_workspace(B, N, H, 128, L_cap, 0) <= cap
+
+
 def test_tree_attn_workspace_plan(lib):
     # Vicuna-7B verify layer: 32 heads, 2048 + 16 keys -> a split plan with workspace
     ws = lib.glide_tree_attn_workspace(1, 16, 32, 128, 2064, 0)
