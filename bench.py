@@ -523,6 +523,10 @@ def main():
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--headline-only", action="store_true",
                     help="skip the other workloads and the streaming probe")
+    ap.add_argument("--verify-only", action="store_true",
+                    help="only run the workload's verification attention calls (warmup + steps "
+                         "eager passes, no timing, no JSON): the launches that counter and trace "
+                         "passes of a profiler summarise")
     ap.add_argument("--calibrate-copy-mib", type=int, default=0,
                     help="only run a plain device-to-device copy of this many MiB (five times), "
                          "for scaling HBM traffic counters; prints nothing else")
@@ -546,6 +550,17 @@ def main():
     glide.load()
 
     wl = W.WORKLOADS[args.workload]
+    if args.verify_only:
+        step = Step(wl, torch.bfloat16, SEED, args.max_splits)
+        if step.probs is not None:
+            glide.cape_expand(step.probs, wl.k, wl.nodes, step.tokens, step.parents, step.n_nodes,
+                              workspace=step.cape_ws)
+        for _ in range(args.warmup + args.steps):
+            step.run_verify_layers()
+        torch.cuda.synchronize()
+        print(json.dumps({"verify_only": wl.name, "passes": args.warmup + args.steps,
+                          "calls": (args.warmup + args.steps) * wl.layers}), flush=True)
+        return
     step, t = measure(wl, args.steps, args.warmup, args.max_splits)
     ms_step, verify_us, planted_ok = t["ms_step"], t["verify_us"], t["planted_ok"]
 
