@@ -401,7 +401,7 @@ def spec_sampling_record(steps, gamma=5, V=32000):
     return out
 
 
-def block_attention_record(steps, B=4, T=2048, H=32, block=5, copies=4):
+def block_attention_record(steps, B=4, T=2048, H=32, block=5, copies=4, eager_only=0):
     """The block-masked cross attention of draft training at a 7B-head
     training shape (4 sequences of 2048 positions, blocks of 5): `copies`
     distinct inputs per graph (1 GB, beyond the last-level cache).  Bound:
@@ -418,6 +418,13 @@ def block_attention_record(steps, B=4, T=2048, H=32, block=5, copies=4):
     def fn():
         for i in range(copies):
             glide.glide_block_attn(qs[i], ks[i], vs[i], outs[i], block)
+    if eager_only:
+        for _ in range(eager_only):
+            fn()
+        torch.cuda.synchronize()
+        print(json.dumps({"only": "block", "passes": eager_only, "calls": eager_only * copies}),
+              flush=True)
+        return None
     fn()
     torch.cuda.synchronize()
     graph = torch.cuda.CUDAGraph()
@@ -523,10 +530,11 @@ def main():
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--headline-only", action="store_true",
                     help="skip the other workloads and the streaming probe")
-    ap.add_argument("--verify-only", action="store_true",
-                    help="only run the workload's verification attention calls (warmup + steps "
-                         "eager passes, no timing, no JSON): the launches that counter and trace "
-                         "passes of a profiler summarise")
+    ap.add_argument("--only", choices=["verify", "block"], default=None,
+                    help="only run warmup + steps eager passes of one part (no timing, no JSON "
+                         "record), for counter and trace passes of a profiler: 'verify' = the "
+                         "workload's verification attention calls, 'block' = the block-masked "
+                         "training attention at the bench's shape")
     ap.add_argument("--calibrate-copy-mib", type=int, default=0,
                     help="only run a plain device-to-device copy of this many MiB (five times), "
                          "for scaling HBM traffic counters; prints nothing else")
@@ -550,7 +558,10 @@ def main():
     glide.load()
 
     wl = W.WORKLOADS[args.workload]
-    if args.verify_only:
+    if args.only == "block":
+        block_attention_record(args.steps, eager_only=args.warmup + args.steps)
+        return
+    if args.only == "verify":
         step = Step(wl, torch.bfloat16, SEED, args.max_splits)
         if step.probs is not None:
             glide.cape_expand(step.probs, wl.k, wl.nodes, step.tokens, step.parents, step.n_nodes,
@@ -558,7 +569,7 @@ def main():
         for _ in range(args.warmup + args.steps):
             step.run_verify_layers()
         torch.cuda.synchronize()
-        print(json.dumps({"verify_only": wl.name, "passes": args.warmup + args.steps,
+        print(json.dumps({"only": "verify", "workload": wl.name, "passes": args.warmup + args.steps,
                           "calls": (args.warmup + args.steps) * wl.layers}), flush=True)
         return
     step, t = measure(wl, args.steps, args.warmup, args.max_splits)

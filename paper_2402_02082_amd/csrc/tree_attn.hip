@@ -650,12 +650,15 @@ void tree_attn_kernel(AttnArgs args) {
 // ring holds kStages steps: while a round is read, the rest are in flight,
 // and the loads of a round go out as soon as the round before it retires.
 //
-// LDS layout of one step: K rows then V rows, 32 rows x 256 B each, stored in
-// 16-byte units with unit (row, chunk) at row * 16 + (chunk ^ (row & 15)).
-// The loads write 64 consecutive units per instruction (four rows, chunks
-// permuted), so each instruction still reads 1 KB of contiguous HBM, and the
-// MFMA-operand reads (16 rows of one chunk, or 16 chunks of one row) hit 16
-// different bank groups.
+// LDS layout of one step: K rows then V rows, 32 rows x 256 B each, in
+// 16-byte units.  K unit (row, chunk) sits at row * 16 + (chunk ^ (row & 15)),
+// V unit (row, chunk) at row * 16 + chunk.  The loads write 64 consecutive
+// units per instruction (four rows; K's chunks permuted), so each instruction
+// still reads 1 KB of contiguous HBM.  The layouts are the ones gfx950's LDS
+// reads without bank conflicts for the two operand patterns: K's reads take
+// 16 rows of one chunk (conflicting 8-way unpermuted), V's take 16 chunks of
+// one row for four rows (measured 2-way conflicting under K's permutation,
+// conflict-free unpermuted).
 //
 // The compiler does not track LDS writes made by memory loads, so the ring
 // is synchronised by hand: each wave waits for its own loads of round r
@@ -678,7 +681,14 @@ __device__ __forceinline__ void ring_wait_and_meet() {
   asm volatile("s_barrier" ::: "memory");
 }
 
-__device__ __forceinline__ int swz_unit(int row, int chunk) { return row * 16 + (chunk ^ (row & 15)); }
+__device__ __forceinline__ int k_unit(int row, int chunk) { return row * 16 + (chunk ^ (row & 15)); }
+__device__ __forceinline__ int v_unit(int row, int chunk) { return row * 16 + chunk; }
+
+// Global-side byte offset of the 16-byte chunk that lane `lane` moves for
+// row `row` of a step: the LDS-DMA writes lane l's 16 bytes to unit l of the
+// instruction's 64, so K lanes fetch the chunk their unit holds.
+__device__ __forceinline__ int dma_k_off(int row, int lane) { return row * 256 + 16 * ((lane & 15) ^ (row & 15)); }
+__device__ __forceinline__ int dma_v_off(int row, int lane) { return row * 256 + 16 * (lane & 15); }
 
 // K and V fragments of one step, read from its LDS copy (layouts as load_kv).
 __device__ __forceinline__ void read_step(Bf16Path::KV& f, const char* stepk, int c, int g) {
@@ -687,10 +697,10 @@ __device__ __forceinline__ void read_step(Bf16Path::KV& f, const char* stepk, in
   for (int kt = 0; kt < 2; ++kt)
 #pragma unroll
     for (int st = 0; st < 4; ++st)
-      f.k[kt][st] = *(const u32x4_t*)(stepk + 16 * swz_unit(16 * kt + c, 4 * st + g));
+      f.k[kt][st] = *(const u32x4_t*)(stepk + 16 * k_unit(16 * kt + c, 4 * st + g));
 #pragma unroll
   for (int i = 0; i < 8; ++i)
-    f.v[i] = *(const u32x4_t*)(stepv + 16 * swz_unit(Bf16Path::key_slot(g, i), c));
+    f.v[i] = *(const u32x4_t*)(stepv + 16 * v_unit(Bf16Path::key_slot(g, i), c));
 }
 
 template <int TQ, int LDS_BYTES, bool TREE>
@@ -735,7 +745,7 @@ void tree_attn_shared_kernel(AttnArgs args) {
   // K or V, i = wave + 4 * (k & 1)) into stage t % kStages; lanes fetch their
   // unit's chunk so the swizzled layout lands in place.
   const int dma_row = 4 * wave + (lane >> 4);
-  const int dma_off = dma_row * 256 + 16 * ((lane & 15) ^ (dma_row & 15));
+  const int dma_off[2] = {dma_k_off(dma_row, lane), dma_v_off(dma_row, lane)};
   auto issue_step = [&](int t) {
     char* stage = ring + (t % kStages) * kStepBytes;
     const int j0 = k_begin + 32 * t;
@@ -744,7 +754,7 @@ void tree_attn_shared_kernel(AttnArgs args) {
       const int m = k / 2, hi = k & 1;
       const __amdgpu_buffer_rsrc_t rs = step_rsrc(m ? vslab : kslab, j0, k_end, 256);
       char* dst = stage + m * (kStepBytes / 2) + (wave + 4 * hi) * 1024;
-      __builtin_amdgcn_raw_ptr_buffer_load_lds(rs, (lds_ptr_t)dst, 16, dma_off + 4096 * hi, 0, 0,
+      __builtin_amdgcn_raw_ptr_buffer_load_lds(rs, (lds_ptr_t)dst, 16, dma_off[m] + 4096 * hi, 0, 0,
                                                kStream);
     }
   };
@@ -1066,7 +1076,7 @@ void block_attn_kernel(BlockAttnArgs args) {
   const char* vslab = (const char*)((const uint16_t*)args.v + head_off);
 
   const int dma_row = 4 * wave + (lane >> 4);
-  const int dma_off = dma_row * 256 + 16 * ((lane & 15) ^ (dma_row & 15));
+  const int dma_off[2] = {dma_k_off(dma_row, lane), dma_v_off(dma_row, lane)};
   auto issue_step = [&](int t, int stage_idx) {
     char* stage = ring + stage_idx * kStepBytes;
     const int j0 = 32 * t;
@@ -1078,7 +1088,7 @@ void block_attn_kernel(BlockAttnArgs args) {
       // default cache policy: every K/V row is read again by the workgroups
       // of the head's later query blocks, and the non-temporal hint of the
       // decode kernels (1.5x the HBM reads here) would evict it from L2
-      __builtin_amdgcn_raw_ptr_buffer_load_lds(rs, (lds_ptr_t)dst, 16, dma_off + 4096 * hi, 0, 0,
+      __builtin_amdgcn_raw_ptr_buffer_load_lds(rs, (lds_ptr_t)dst, 16, dma_off[m] + 4096 * hi, 0, 0,
                                                kKeep);
     }
   };
