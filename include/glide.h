@@ -270,7 +270,7 @@ int glide_verify_commit(const float* logits, int V, const int32_t* cand_tokens,
  *   a   [M, K] bfloat16, 16-byte aligned;  w_t [N, K] bfloat16, 16-byte
  *       aligned;  out [M, N] of out_dtype (GLIDE_BF16 rounds to nearest
  *       even, GLIDE_F32 keeps the float32 accumulation).
- *   M >= 1 (64 rows per launch, more rows take further launches, each
+ *   M >= 1 (128 rows per launch, more rows take further launches, each
  *   reading w_t again); 8 <= K <= 2^20 with K % 8 == 0; N >= 1.
  */
 int glide_rows_matmul(const void* a, const void* w_t, void* out, int M, int K, int N,

@@ -20,7 +20,7 @@ hipError_t launch_argmax_rows(const float* logits, int rows, int V, int32_t* idx
 
 // out[m, n] = sum_k a[m, k] w_t[n, k] (bf16 in, fp32 accumulation); up to
 // kMaxMatmulRows rows per launch, more rows loop.
-constexpr int kMaxMatmulRows = 64;
+constexpr int kMaxMatmulRows = 128;
 constexpr int kMaxMatmulK = 1 << 20;
 hipError_t launch_rows_matmul(const void* a, const void* w, void* out, int M, int K, int N,
                               bool out_bf16, bool packed, hipStream_t stream);

@@ -5,14 +5,15 @@
 //
 //   out[m, n] = sum_k a[m, k] * w_t[n, k]      a [M, K], w_t [N, K] (bf16)
 //
-// With M <= 64 rows the weights dominate the bytes (every weight element is
+// With M <= 128 rows the weights dominate the bytes (every weight element is
 // used M times), so the kernel streams w_t once: one workgroup per 16 output
 // features, its four waves taking interleaved 32-wide K steps.  Each step is
 // one v_mfma_f32_16x16x32_bf16 per 16-row tile of `a`, with A = 16 rows of
 // w_t (16 contiguous bytes per lane) and B = the matching rows of `a` -- the
 // same operand shapes as the attention kernel's K * Q^T.  Loads go through
 // range-checked buffer descriptors (weight rows past N and activation rows
-// past M read as zeros), eight steps in flight per wave in registers.
+// past M read as zeros), five to eight steps in flight per wave in
+// registers.
 //
 // An operand tile spans 16 weight rows, so from a row-major w_t each load
 // instruction fetches 64 bytes from each of 16 rows K * 2 bytes apart.  The
@@ -34,7 +35,11 @@ typedef __attribute__((ext_vector_type(4))) uint32_t u32x4_t;
 typedef __attribute__((ext_vector_type(8))) __bf16 bf16x8_t;
 
 constexpr int kWaves = 4;
-constexpr int kBufs = 8;             // K steps in flight per wave
+// K steps in flight per wave: eight while a step's registers are small; a
+// step of MT activation tiles holds (1 + MT) x 16 bytes per lane, so larger
+// row counts keep fewer in flight (at most 256 registers: two waves per SIMD).
+template <int MT>
+constexpr int bufs_for() { return MT <= 4 ? 8 : (MT <= 6 ? 6 : 5); }
 constexpr uint32_t kDesc3 = 0x00020000u;
 constexpr int kStream = 2;           // weights are read once: non-temporal
 constexpr int kOutOfRange = 1 << 30; // past every descriptor (M * K * 2 < 2^30)
@@ -78,7 +83,8 @@ __device__ __forceinline__ void store_out(uint16_t* p, float v) {
 }
 
 template <int MT, class OutT, bool PACKED>
-__global__ __launch_bounds__(64 * kWaves) void rows_matmul_kernel(const uint16_t* __restrict__ a,
+__global__ __launch_bounds__(64 * kWaves) __attribute__((amdgpu_waves_per_eu(MT > 4 ? 2 : 1)))
+void rows_matmul_kernel(const uint16_t* __restrict__ a,
                                                                   const uint16_t* __restrict__ w_t,
                                                                   OutT* __restrict__ out, int M,
                                                                   int K, int N) {
@@ -102,6 +108,7 @@ __global__ __launch_bounds__(64 * kWaves) void rows_matmul_kernel(const uint16_t
   const int a_off = c * K * 2;       // B operand: activation row 16 t + c
   const int a_tile_stride = 16 * K * 2;
 
+  constexpr int kBufs = bufs_for<MT>();
   const int steps = (K + 31) / 32;
   const int my_steps = steps > wave ? (steps - wave + kWaves - 1) / kWaves : 0;
   const int iters = (my_steps + kBufs - 1) / kBufs;
@@ -156,14 +163,16 @@ hipError_t launch_rows(const uint16_t* a, const uint16_t* w_t, OutT* out, int M,
                        hipStream_t stream) {
   const dim3 grid((N + 15) / 16), block(64 * kWaves);
   const int mt = (M + 15) / 16;
-  if (mt == 1)
-    hipLaunchKernelGGL((rows_matmul_kernel<1, OutT, PACKED>), grid, block, 0, stream, a, w_t, out, M, K, N);
-  else if (mt == 2)
-    hipLaunchKernelGGL((rows_matmul_kernel<2, OutT, PACKED>), grid, block, 0, stream, a, w_t, out, M, K, N);
-  else if (mt == 3)
-    hipLaunchKernelGGL((rows_matmul_kernel<3, OutT, PACKED>), grid, block, 0, stream, a, w_t, out, M, K, N);
-  else
-    hipLaunchKernelGGL((rows_matmul_kernel<4, OutT, PACKED>), grid, block, 0, stream, a, w_t, out, M, K, N);
+  switch (mt) {
+    case 1: hipLaunchKernelGGL((rows_matmul_kernel<1, OutT, PACKED>), grid, block, 0, stream, a, w_t, out, M, K, N); break;
+    case 2: hipLaunchKernelGGL((rows_matmul_kernel<2, OutT, PACKED>), grid, block, 0, stream, a, w_t, out, M, K, N); break;
+    case 3: hipLaunchKernelGGL((rows_matmul_kernel<3, OutT, PACKED>), grid, block, 0, stream, a, w_t, out, M, K, N); break;
+    case 4: hipLaunchKernelGGL((rows_matmul_kernel<4, OutT, PACKED>), grid, block, 0, stream, a, w_t, out, M, K, N); break;
+    case 5: hipLaunchKernelGGL((rows_matmul_kernel<5, OutT, PACKED>), grid, block, 0, stream, a, w_t, out, M, K, N); break;
+    case 6: hipLaunchKernelGGL((rows_matmul_kernel<6, OutT, PACKED>), grid, block, 0, stream, a, w_t, out, M, K, N); break;
+    case 7: hipLaunchKernelGGL((rows_matmul_kernel<7, OutT, PACKED>), grid, block, 0, stream, a, w_t, out, M, K, N); break;
+    default: hipLaunchKernelGGL((rows_matmul_kernel<8, OutT, PACKED>), grid, block, 0, stream, a, w_t, out, M, K, N); break;
+  }
   return hipGetLastError();
 }
 
@@ -202,7 +211,8 @@ hipError_t launch_pack_rows_weights(const void* w_t, void* packed, int K, int N,
 
 hipError_t launch_rows_matmul(const void* a, const void* w, void* out, int M, int K, int N,
                               bool out_bf16, bool packed, hipStream_t stream) {
-  // at most 64 activation rows per launch; more rows take further launches
+  // at most kMaxMatmulRows activation rows per launch; more rows take
+  // further launches, each streaming the weights again
   for (int m0 = 0; m0 < M; m0 += kMaxMatmulRows) {
     const int rows = min(kMaxMatmulRows, M - m0);
     const uint16_t* ap = (const uint16_t*)a + (size_t)m0 * K;

@@ -32,7 +32,8 @@ def _bf16(shape, seed, scale=1.0):
 
 
 @pytest.mark.parametrize("M,K,N", [(1, 8, 1), (5, 4096, 4096), (16, 4096, 4096), (17, 512, 100),
-                                   (64, 1024, 333), (130, 256, 48), (3, 4104, 16), (5, 96, 4096)])
+                                   (64, 1024, 333), (80, 4096, 4096), (97, 520, 200), (128, 256, 48),
+                                   (130, 256, 48), (257, 64, 17), (3, 4104, 16), (5, 96, 4096)])
 @pytest.mark.parametrize("out_dtype", [torch.float32, torch.bfloat16])
 def test_rows_matmul(M, K, N, out_dtype):
     require_gpu()
@@ -106,7 +107,8 @@ def test_cross_block_workload(cfg):
 
 
 @pytest.mark.parametrize("M,K,N", [(1, 8, 1), (5, 4096, 4096), (17, 512, 100), (64, 1024, 333),
-                                   (130, 256, 48), (3, 4104, 16), (5, 40, 4097)])
+                                   (80, 4096, 4096), (113, 200, 33), (130, 256, 48), (3, 4104, 16),
+                                   (5, 40, 4097)])
 @pytest.mark.parametrize("out_dtype", [torch.float32, torch.bfloat16])
 def test_rows_matmul_packed(M, K, N, out_dtype):
     """Packed weights: the same registers reach the matrix cores, so the
@@ -169,3 +171,29 @@ def test_cross_block_packed(B, Nq, H, d_D, L_cap, lens):
                           store=torch.bfloat16)
     excess = bf16_ok(to64(got), want)
     assert excess <= 0, excess
+
+
+@pytest.mark.parametrize("M", [80, 128])
+def test_rows_matmul_one_pass_matches_row_blocks(M):
+    """Up to 128 rows go through one launch; each output row is the same
+    dot products in the same order whatever the other rows, so the one-pass
+    result equals, bit for bit, the projections of the rows taken 64 and
+    then M - 64 at a time (row-major and packed weights)."""
+    require_gpu()
+    say("rows_matmul one pass", dict(M=M))
+    K, N = 4096, 1024
+    a = _bf16((M, K), 41 + M).cuda()
+    w_t = _bf16((N, K), 42, 1.0 / np.sqrt(K)).cuda()
+    packed = glide.pack_rows_weights(w_t)
+    for out_dtype in (torch.bfloat16, torch.float32):
+        view = torch.int16 if out_dtype == torch.bfloat16 else torch.int32
+        one = torch.full((M, N), float("nan"), dtype=out_dtype, device="cuda")
+        parts = torch.full((M, N), float("nan"), dtype=out_dtype, device="cuda")
+        glide.glide_rows_matmul(a, w_t, one)
+        glide.glide_rows_matmul(a[:64].contiguous(), w_t, parts[:64])
+        glide.glide_rows_matmul(a[64:].contiguous(), w_t, parts[64:])
+        onep = torch.full_like(one, float("nan"))
+        glide.glide_rows_matmul_packed(a, packed, onep)
+        torch.cuda.synchronize()
+        assert torch.equal(one.view(view), parts.view(view))
+        assert torch.equal(onep.view(view), one.view(view))
