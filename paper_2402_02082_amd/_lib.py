@@ -12,7 +12,9 @@ import os
 import torch
 
 _PKG = os.path.dirname(os.path.abspath(__file__))
-LIB_PATH = os.path.join(_PKG, "libglide.so")
+# GLIDE_LIBRARY selects another build of the same library (for instance the
+# AddressSanitizer build, libglide_asan.so).
+LIB_PATH = os.environ.get("GLIDE_LIBRARY") or os.path.join(_PKG, "libglide.so")
 
 GLIDE_OK, GLIDE_EINVAL, GLIDE_ERANGE, GLIDE_EHIP, GLIDE_ESCRATCH = 0, 1, 2, 3, 4
 GLIDE_BF16, GLIDE_F32 = 0, 1

@@ -35,10 +35,20 @@ def hipcc():
     return path
 
 
-def build(verbose=False):
-    """Compile every source into paper_2402_02082_amd/libglide.so (always rebuilds)."""
-    tmp = LIB + ".tmp"
-    cmd = [hipcc(), *HIPCC_FLAGS, "-I", INCLUDE, "-I", CSRC,
+LIB_ASAN = os.path.join(PKG, "libglide_asan.so")
+# AddressSanitizer on the host code only (argument checks, planning, launch
+# set-up); the GPU code is built as usual.
+ASAN_FLAGS = ["-Xarch_host", "-fsanitize=address", "-Xarch_host", "-fno-omit-frame-pointer", "-g"]
+
+
+def build(verbose=False, asan=False):
+    """Compile every source into paper_2402_02082_amd/libglide.so (always
+    rebuilds); with asan=True into libglide_asan.so, host code instrumented
+    with AddressSanitizer (load it with GLIDE_LIBRARY and the sanitizer
+    runtime preloaded)."""
+    lib = LIB_ASAN if asan else LIB
+    tmp = lib + ".tmp"
+    cmd = [hipcc(), *HIPCC_FLAGS, *(ASAN_FLAGS if asan else []), "-I", INCLUDE, "-I", CSRC,
            *[os.path.join(CSRC, s) for s in SOURCES], "-o", tmp]
     if verbose:
         print(" ".join(cmd), flush=True)
@@ -49,9 +59,9 @@ def build(verbose=False):
         raise RuntimeError("hipcc failed:\n" + err)
     if verbose and err.strip():
         print(err, file=sys.stderr)
-    os.replace(tmp, LIB)
-    return LIB
+    os.replace(tmp, lib)
+    return lib
 
 
 if __name__ == "__main__":
-    print(build(verbose=True))
+    print(build(verbose=True, asan="--asan" in sys.argv[1:]))
