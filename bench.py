@@ -146,37 +146,68 @@ class Step:
                                   max_splits=self.max_splits, workspace=self.xws)
 
 
-def cpu_baseline(step, budget_s=12.0):
+def host_cores():
+    """Host threads the oracle may use on this machine: the CPUs this process
+    may run on, capped by the OMP_NUM_THREADS share the machine sets (a GPU
+    box gives each GPU's jobs a share of its cores), and the CPU model."""
+    affinity = len(os.sched_getaffinity(0))
+    share = int(os.environ.get("OMP_NUM_THREADS", "0") or 0)
+    threads = min(affinity, share) if share > 0 else affinity
+    model = "unknown"
+    try:
+        for line in open("/proc/cpuinfo"):
+            if line.startswith("model name"):
+                model = line.split(":", 1)[1].strip()
+                break
+    except OSError:
+        pass
+    return {"threads": threads, "affinity_cores": affinity, "omp_num_threads": share or None,
+            "cpu_model": model}
+
+
+def _bits(t):
+    return t.view(torch.int16 if t.dtype == torch.bfloat16 else torch.int32).cpu().numpy()
+
+
+def _f64(t):
+    return t.float().cpu().numpy().astype(np.float64)
+
+
+def oracle_integer_steps(step):
+    """The float64 oracle's CaPE expansion and verification epilogue (argmax,
+    acceptance, commit of every layer's cache), in full; returns (seconds,
+    parents the attention uses)."""
+    from oracle import cape as OC
+    from oracle import commit as OCm
+    wl = step.wl
+    k_bits = [_bits(k) for k in step.k_caches]
+    v_bits = [_bits(v) for v in step.v_caches]
+    t0 = time.perf_counter()
+    if wl.tree == "cape":
+        tokens, parents, _ = OC.cape_expand(step.probs_np, wl.k, wl.nodes)
+    else:
+        tokens = step.chain_tokens.cpu().numpy()
+        parents = step.chain_parents.cpu().numpy()
+    OCm.verify_commit(step.logits_np, tokens, parents, step.lens_np, k_bits, v_bits)
+    return time.perf_counter() - t0, parents
+
+
+def cpu_baseline(step, threads, budget_s=12.0):
     """The float64 oracle on a bounded sample of the same step: the CaPE
     expansion and the verification epilogue (argmax, acceptance, commit of
     every layer's cache) in full, then verification-attention layers (all
-    heads) until ~budget_s, then the cross-attention layer.  Reported in the
-    metric's unit (attention GB/s) with the BLAS threads used."""
+    heads) until ~budget_s, then the cross-attention layer; at `threads`
+    BLAS threads.  Reported in the metric's unit (attention GB/s)."""
     import threadpoolctl
 
     from oracle import attention as OA
-    from oracle import cape as OC
-    from oracle import commit as OCm
 
     wl = step.wl
-    f64 = lambda t: t.float().cpu().numpy().astype(np.float64)  # noqa: E731
-    bits = lambda t: t.view(torch.int16 if t.dtype == torch.bfloat16 else torch.int32).cpu().numpy()  # noqa: E731
-    k_bits = [bits(k) for k in step.k_caches]
-    v_bits = [bits(v) for v in step.v_caches]
-    with threadpoolctl.threadpool_limits(1):
-        t0 = time.perf_counter()
-        if wl.tree == "cape":
-            tokens, parents, _ = OC.cape_expand(step.probs_np, wl.k, wl.nodes)
-        else:
-            tokens = step.chain_tokens.cpu().numpy()
-            parents = step.chain_parents.cpu().numpy()
-        OCm.verify_commit(step.logits_np, tokens, parents, step.lens_np, k_bits, v_bits)
-        t_int = time.perf_counter() - t0
-    del k_bits, v_bits
-    with threadpoolctl.threadpool_limits(1):
+    with threadpoolctl.threadpool_limits(threads):
+        t_int, parents = oracle_integer_steps(step)
         t_attn, nbytes, layers_done = 0.0, 0, 0
         for (q, k, v) in step.layers:
-            qh, kh, vh = f64(q), f64(k), f64(v)
+            qh, kh, vh = _f64(q), _f64(k), _f64(v)
             t1 = time.perf_counter()
             OA.tree_attention(qh, kh, vh, step.lens_np, parents)
             t_attn += time.perf_counter() - t1
@@ -187,16 +218,75 @@ def cpu_baseline(step, budget_s=12.0):
         if wl.cross:
             _, k, v = step.layers[-1]
             t1 = time.perf_counter()
-            OA.tree_attention(f64(step.cross_q), f64(k), f64(v), step.lens_np, None)
+            OA.tree_attention(_f64(step.cross_q), _f64(k), _f64(v), step.lens_np, None)
             t_attn += time.perf_counter() - t1
             nbytes += step.cross_bytes
     total = t_attn + t_int
-    return {"value": round(nbytes / total / 1e9, 6), "unit": "GB/s", "cores": 1, "kind": "oracle",
+    return {"value": round(nbytes / total / 1e9, 6), "unit": "GB/s", "cores": threads,
+            "kind": "oracle",
             "sample": "%s: CaPE expansion and the verification epilogue (argmax, acceptance, "
-                      "commit of every layer) in full, %d of %d "
-                      "verification-attention layers (all heads)%s, float64 NumPy, %.1f s"
+                      "commit of every layer) in full, %d of %d verification-attention layers "
+                      "(all heads)%s, float64 NumPy, %d BLAS thread(s), %.1f s"
                       % (wl.name, layers_done, wl.layers, " + the cross-attention layer"
-                         if wl.cross else "", total)}
+                         if wl.cross else "", threads, total)}
+
+
+def oracle_sampled(step, threads, budget_s=5.0):
+    """The oracle's time for a workload too large to run in full on the host:
+    the integer steps in full, and verification attention on the
+    deterministic sample of (sequence, head) units -- every sequence, the
+    first and last layer, heads 0, H/2 and H - 1, in that order until
+    ~budget_s of attention time -- extrapolated to the whole step (mean time
+    per unit x sequences x layers x heads, and the cross layer's units
+    likewise).  Labelled extrapolated."""
+    import threadpoolctl
+
+    from oracle import attention as OA
+
+    wl = step.wl
+    heads = sorted({0, wl.heads // 2, wl.heads - 1})
+    layers = sorted({0, wl.layers - 1})
+    units = [(b, l, h) for l in layers for h in heads for b in range(wl.batch)]
+    with threadpoolctl.threadpool_limits(threads):
+        t_int, parents = oracle_integer_steps(step)
+        t_units, done = 0.0, 0
+        for b, l, h in units:
+            q, k, v = step.layers[l]
+            L = int(step.lens_np[b])
+            rows = L + wl.nodes
+            qh, kh, vh = _f64(q[b, :, h]), _f64(k[b, h, :rows]), _f64(v[b, h, :rows])
+            t1 = time.perf_counter()
+            OA.tree_attention_head(qh, kh, vh, L, parents[b])
+            t_units += time.perf_counter() - t1
+            done += 1
+            if t_units > budget_s:
+                break
+        per_unit = t_units / done
+        total_units = wl.batch * wl.layers * wl.heads
+        t_cross, cross_done = 0.0, 0
+        if wl.cross:
+            _, k, v = step.layers[-1]
+            for b, _, h in [u for u in units if u[1] == layers[-1]]:
+                L = int(step.lens_np[b])
+                qh, kh, vh = _f64(step.cross_q[b, :, h]), _f64(k[b, h, :L]), _f64(v[b, h, :L])
+                t1 = time.perf_counter()
+                OA.tree_attention_head(qh, kh, vh, L, None)
+                t_cross += time.perf_counter() - t1
+                cross_done += 1
+                if t_cross > budget_s / 2:
+                    break
+    seconds = t_int + per_unit * total_units
+    nbytes = step.verify_bytes * wl.layers
+    if cross_done:
+        seconds += t_cross / cross_done * wl.batch * wl.heads
+        nbytes += step.cross_bytes
+    return {"value": round(nbytes / seconds / 1e9, 6), "unit": "GB/s", "cores": threads,
+            "kind": "oracle", "extrapolated": True, "seconds_per_step": round(seconds, 3),
+            "sample": "%s: integer steps in full (%.2f s); verification attention on %d of "
+                      "%d (sequence, layer, head) units (every sequence x first/last layer x "
+                      "heads 0, H/2, H-1), %.3f s per unit, extrapolated to %d units%s"
+                      % (wl.name, t_int, done, len(units), per_unit, total_units,
+                         "; cross attention %d units" % cross_done if cross_done else "")}
 
 
 def kernel_source_hash():
@@ -206,10 +296,17 @@ def kernel_source_hash():
     return hashlib.sha256(src).hexdigest()[:16]
 
 
-def load_traffic():
-    """HBM bytes per verification attention call from the committed rocprofv3
-    counter summary, or None when the kernel source changed since then."""
-    path = os.path.join(ROOT, "profiles", "tree_attn_vicuna7b_pmc.json")
+# Stem of each workload's profile summaries under profiles/.
+PROFILE_STEM = {"7b-1layer-chain5": "chain5", "vicuna7b-cape16": "vicuna7b",
+                "vicuna13b-cape32": "vicuna13b", "vicuna33b-cape64": "vicuna33b",
+                "7b-longctx-cape64": "longctx"}
+
+
+def load_traffic(wl_name="vicuna7b-cape16"):
+    """HBM bytes per verification attention call of a workload from the
+    committed rocprofv3 counter summary, or None when there is none or the
+    kernel source changed since it was taken."""
+    path = os.path.join(ROOT, "profiles", "tree_attn_%s_pmc.json" % PROFILE_STEM.get(wl_name, wl_name))
     if not os.path.exists(path):
         return None
     try:
@@ -465,9 +562,12 @@ def speedup_model(verify_us, cross_block):
     return rec
 
 
-def other_configs(skip, steps, warmup, max_splits):
+def other_configs(skip, steps, warmup, max_splits, oracle_threads=None):
     """The verification step and the whole step of every other workload,
-    measured as the headline one (same seed, graphs, events)."""
+    measured as the headline one (same seed, graphs, events); with
+    oracle_threads, the float64 oracle's time beside it (the one-layer
+    workload in full at that many threads and at one, the others on their
+    extrapolated sample)."""
     out = []
     for i in sorted(W.WORKLOADS):
         if i == skip:
@@ -476,6 +576,14 @@ def other_configs(skip, steps, warmup, max_splits):
         step, t = measure(wl, steps, warmup, max_splits)
         vgbps = step.verify_bytes * wl.layers / (t["verify_us"] * 1e-6) / 1e9
         sbytes = step.verify_bytes * wl.layers + step.cross_bytes
+        traffic = load_traffic(wl.name)
+        oracle = None
+        if oracle_threads:
+            if wl.layers == 1:
+                oracle = cpu_baseline(step, oracle_threads, budget_s=30.0)
+                oracle["one_thread"] = cpu_baseline(step, 1, budget_s=30.0)
+            else:
+                oracle = oracle_sampled(step, oracle_threads)
         out.append({"workload": wl.name, "layers": wl.layers, "batch": wl.batch,
                     "tree_nodes": wl.nodes,
                     "us_per_verify_step": round(t["verify_us"], 2),
@@ -485,8 +593,12 @@ def other_configs(skip, steps, warmup, max_splits):
                     "ms_per_step": round(t["ms_step"], 4),
                     "step_gbps": round(sbytes / (t["ms_step"] * 1e-3) / 1e9, 1),
                     "planted_accept_len_ok": t["planted_ok"],
+                    "verify_call_bytes": step.verify_bytes,
+                    "verify_call_traffic": traffic,
+                    "verify_call_traffic_ratio": round(traffic / step.verify_bytes, 4) if traffic else None,
                     "verify_commit": commit_record(step, t),
-                    "cross_block": cross_block_record(step, steps) if wl.cross else None})
+                    "cross_block": cross_block_record(step, steps) if wl.cross else None,
+                    "oracle": oracle})
         del step
         torch.cuda.empty_cache()
     return out
@@ -611,7 +723,7 @@ def main():
         "block_attention": block_attention_record(max(3, min(args.steps, 10))),
         "roofline": {"bound": "hbm", "achieved": round(achieved, 2), "peak": HBM_PEAK_GBPS,
                      "unit": "GB/s", "frac": round(achieved / HBM_PEAK_GBPS, 4),
-                     "traffic": load_traffic(),
+                     "traffic": load_traffic(wl.name),
                      "kernel": "glide_tree_attn call (tree_attn_kernel + tree_attn_combine), "
                                "verification layer",
                      "bytes_per_launch": step.verify_bytes,
@@ -620,13 +732,17 @@ def main():
                                "step's calls, divided by the call count"},
     }
     rec["speedup_model"] = speedup_model(verify_us, rec["cross_block"])
+    host = host_cores()
     if not args.no_cpu_baseline:
-        rec["cpu_baseline"] = cpu_baseline(step)
+        rec["cpu_baseline"] = cpu_baseline(step, host["threads"])
+        rec["cpu_baseline"]["host"] = host
+        rec["cpu_baseline"]["one_thread"] = cpu_baseline(step, 1)
     if not args.headline_only:
         del step
         torch.cuda.empty_cache()
         rec["other_configs"] = other_configs(args.workload, max(3, min(args.steps, 10)),
-                                             max(1, min(args.warmup, 2)), args.max_splits)
+                                             max(1, min(args.warmup, 2)), args.max_splits,
+                                             None if args.no_cpu_baseline else host["threads"])
         rec["stream_probe"] = stream_probe()
     print(json.dumps(rec), flush=True)
 
