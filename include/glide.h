@@ -87,11 +87,18 @@ int glide_last_hip_error(void);
 /*
  * Workspace bytes glide_tree_attn needs for these sizes (0 when the call runs
  * without a workspace, i.e. with one split).  Arguments as glide_tree_attn.
- * The workspace holds the per-split partial softmax states (running max,
- * running sum and unnormalised output of every query row); each call writes
- * them before reading them, so no initialisation is needed and one buffer of
+ * The workspace starts with a fixed 256 KiB block of arrival counters (one per
+ * (sequence, head), 128 bytes apart), followed by the per-split partial
+ * softmax states (running max, running sum and unnormalised output of every
+ * query row).  The workgroup of a split counts itself in once its states are
+ * written, and the one that completes a (sequence, head) merges them, so a
+ * call is a single launch.  The counter block must be zero before the
+ * workspace's first use (zero-fill the whole buffer once); every call leaves
+ * it zero, and the partial states need no initialisation, so one buffer of
  * the largest size needed can serve calls of any shape in turn.  It must not
- * be shared by calls that can run concurrently.  Returns 0 for invalid sizes.
+ * be shared by calls that can run concurrently.  (Calls with B * H > 2048
+ * merge in a second launch and do not use the counters.)  Returns 0 for
+ * invalid sizes.
  */
 size_t glide_tree_attn_workspace(int B, int N, int H, int D, int L_cap,
                                  int max_splits);
@@ -138,13 +145,15 @@ int glide_tree_attn(const void* q, const void* k_cache, const void* v_cache,
  * allocate device memory (code under HIP graph capture, tight serving loops,
  * harnesses that forbid allocation).  Same arguments, same kernels and the
  * same results as glide_tree_attn with max_splits alike, but no workspace
- * argument: the split partial states live in a fixed scratch array of
- * glide_tree_attn_noalloc_max_workspace() bytes (16 MiB) that the library
- * holds on every GPU it runs on until the process ends.  The call allocates
- * nothing and records no memset (the partials are written before they are
- * read).  Sizes whose split plan needs more than the scratch holds
- * (glide_tree_attn_workspace(...) > the maximum) return GLIDE_ESCRATCH
- * before any HIP call; sizes that need no workspace never touch it.
+ * argument: the arrival counters and split partial states live in a fixed
+ * scratch array of glide_tree_attn_noalloc_max_workspace() bytes (16 MiB)
+ * that the library holds on every GPU it runs on until the process ends.
+ * The call allocates nothing and records no memset: the array starts zeroed
+ * when the library is loaded, every call leaves its counters zero, and the
+ * partials are written before they are read.  Sizes whose split plan needs
+ * more than the scratch holds (glide_tree_attn_workspace(...) > the maximum)
+ * return GLIDE_ESCRATCH before any HIP call; sizes that need no workspace
+ * never touch it.
  * The first call on a device, with that device current, looks up the
  * scratch array's device address (hipGetSymbolAddress).
  * Every call on one GPU shares that GPU's scratch: calls that can overlap on
@@ -313,8 +322,10 @@ int glide_rows_matmul_packed(const void* a, const void* w_packed, void* out, int
  *   k_cache, v_cache [B, H, L_cap, D];  seq_lens [B] int32;
  *   wo_t [d_D, H*D] (the transpose of W^O);  out [B, Nq, d_D].
  *   D == 128; 1 <= Nq <= 64; d_D % 8 == 0; scale <= 0 means 1/sqrt(D);
- *   workspace of glide_cross_block_workspace() bytes, 16-byte aligned,
- *   needing no initialisation (0 for invalid sizes).
+ *   workspace of glide_cross_block_workspace() bytes, 16-byte aligned (0 for
+ *   invalid sizes); it begins with the attention's workspace, so its first
+ *   256 KiB must be zero before its first use, and every call leaves them so
+ *   (see glide_tree_attn_workspace).
  */
 size_t glide_cross_block_workspace(int B, int Nq, int d_D, int H, int D, int L_cap);
 int glide_cross_block(const void* hidden, const void* wq_t, const void* k_cache,

@@ -24,7 +24,7 @@ PyTorch only provides device memory and streams.
 """
 
 from ._lib import (  # noqa: F401
-    CAPE_MAX_K, GLIDE_BF16, GLIDE_EHIP, GLIDE_EINVAL, GLIDE_ERANGE, GLIDE_ESCRATCH, GLIDE_F32,
+    ATTN_COUNTER_BYTES, CAPE_MAX_K, GLIDE_BF16, GLIDE_EHIP, GLIDE_EINVAL, GLIDE_ERANGE, GLIDE_ESCRATCH, GLIDE_F32,
     GLIDE_OK,
     HEAD_DIM, MAX_NODES, MAX_SPLITS, GlideError, attn_workspace, cape_expand,
     cross_block_workspace, glide_argmax_rows, glide_block_attn, glide_cross_block,

@@ -128,17 +128,25 @@ def _dev(t, name, dtype=None):
         _need(t.dtype == dtype, "%s must be %s" % (name, dtype))
 
 
-def _alloc_bytes(nbytes, device, stream=None):
+def _alloc_bytes(nbytes, device, stream=None, zero=False):
     """A byte buffer allocated on the stream that will use it.  torch's caching
     allocator ties a block to the stream current at allocation and reuses it
     for that stream's later work once freed; a buffer used on another stream
     must be allocated there, or its memory could be handed to the current
-    stream's work while the kernels on `stream` still use it."""
+    stream's work while the kernels on `stream` still use it.  zero=True
+    fills it with zeros (on that stream): attention workspaces keep arrival
+    counters that must start at zero, and every call leaves them so."""
+    make = torch.zeros if zero else torch.empty
     if stream is None:
-        return torch.empty(nbytes, dtype=torch.uint8, device=device)
+        return make(nbytes, dtype=torch.uint8, device=device)
     with torch.cuda.stream(stream):
-        return torch.empty(nbytes, dtype=torch.uint8, device=device)
+        return make(nbytes, dtype=torch.uint8, device=device)
 
+
+# Bytes of the arrival-counter block at the start of every attention
+# workspace (include/glide.h, glide_tree_attn_workspace): zero before the
+# first call, left zero by every call.
+ATTN_COUNTER_BYTES = 2048 * 128
 
 # Workspaces, kept per (device, stream) so that calls that may run
 # concurrently on different streams never share partial states.  Each is
@@ -155,7 +163,7 @@ def attn_workspace(B, N, H, L_cap, max_splits, device, stream=None):
     key = (str(device), s.cuda_stream)
     ws = _ws_cache.get(key)
     if ws is None or ws.numel() < need:
-        ws = _alloc_bytes(need, device, s)
+        ws = _alloc_bytes(need, device, s, zero=True)
         _ws_cache[key] = ws
     return ws
 
@@ -376,7 +384,7 @@ def glide_rows_matmul_packed(a, w_packed, out, stream=None):
 def cross_block_workspace(B, Nq, d_D, H, L_cap, device, stream=None):
     need = load().glide_cross_block_workspace(B, Nq, d_D, H, HEAD_DIM, L_cap)
     _need(need > 0, "unsupported cross-attention block sizes")
-    return _alloc_bytes(need, device, stream)
+    return _alloc_bytes(need, device, stream, zero=True)
 
 
 def glide_cross_block(hidden, wq_t, k_cache, v_cache, seq_lens, wo_t, out, scale=0.0,

@@ -82,6 +82,7 @@ glide::AttnArgs attn_args(const void* q, const void* k_cache, const void* v_cach
   char* ws = (char*)workspace;
   a.part_o = plan.ws_bytes ? (float*)(ws + plan.part_o_off) : nullptr;
   a.part_ml = plan.ws_bytes ? (float2*)(ws + plan.part_ml_off) : nullptr;
+  a.counters = plan.ws_bytes && plan.merge_in_kernel ? (unsigned*)(ws + plan.counters_off) : nullptr;
   a.B = B;
   a.N = N;
   a.H = H;
@@ -105,8 +106,9 @@ size_t align256(size_t n) { return (n + 255) & ~(size_t)255; }
 // grid dimension (at most 65535).
 bool cape_rows_ok(int B, int gamma) { return (long)B * gamma <= 65535; }
 
-// Workspace of the cross-attention block: projected queries, concatenated
-// heads (both bf16 [B, Nq, H, D]) and the attention's split partials.
+// Workspace of the cross-attention block: the attention's split workspace
+// first (so its arrival counters sit at offset 0 whatever the shape), then
+// the projected queries and the concatenated heads (both bf16 [B, Nq, H, D]).
 struct CrossPlan {
   glide::AttnPlan attn;
   size_t q_off, heads_off, attn_off, bytes;
@@ -117,10 +119,10 @@ bool cross_block_plan(int B, int Nq, int d_D, int H, int D, int L_cap, CrossPlan
   if (!rows_matmul_sizes_ok(B * Nq, d_D, H * D) || (double)B * Nq > 1.0e9) return false;
   p->attn = glide::plan_tree_attn(B, Nq, H, L_cap, 0);
   const size_t rows = align256((size_t)B * Nq * H * D * 2);
-  p->q_off = 0;
-  p->heads_off = rows;
-  p->attn_off = 2 * rows;
-  p->bytes = 2 * rows + p->attn.ws_bytes;
+  p->attn_off = 0;
+  p->q_off = align256(p->attn.ws_bytes);
+  p->heads_off = p->q_off + rows;
+  p->bytes = p->heads_off + rows;
   return true;
 }
 

@@ -14,12 +14,24 @@ constexpr int kNumCU = 256;        // MI355X compute units (split heuristic)
 constexpr int kChunkQuantum = 32;  // split boundaries are multiples of this
 constexpr int kMinChunk = 128;     // smallest split the automatic plan makes
 
+// Arrival counters of the in-kernel split merge: one per (sequence, head),
+// 128 bytes apart (counters sharing a cache line serialise their atomics),
+// in a fixed block at offset 0 of every split workspace, so a buffer that
+// serves calls of different shapes never finds partial states where a later
+// call keeps counters.  The block must be zero before a workspace's first
+// use; every call leaves it zero.  Calls with more (sequence, head) pairs
+// than slots merge in a second launch instead.
+constexpr int kCounterSlots = 2048;
+constexpr int kCounterStride = 32;  // uint32 words: 128 bytes
+constexpr size_t kCounterBytes = (size_t)kCounterSlots * kCounterStride * 4;
+
 // How the keys of one (sequence, head) are divided between workgroups.
 struct AttnPlan {
   int splits;       // workgroups per (sequence, head)
   int chunk;        // keys per workgroup (multiple of kChunkQuantum)
-  size_t ws_bytes;  // workspace for the partial states (0 if splits == 1)
-  size_t part_o_off, part_ml_off;
+  size_t ws_bytes;  // workspace: counters + partial states (0 if splits == 1)
+  size_t counters_off, part_o_off, part_ml_off;
+  bool merge_in_kernel;  // the last split to finish merges (else a second launch)
 };
 
 AttnPlan plan_tree_attn(int B, int N, int H, int L_cap, int max_splits);
@@ -33,6 +45,7 @@ struct AttnArgs {
   void* out;
   float* part_o;           // [B, H, splits, N, D]
   float2* part_ml;         // [B, H, splits, N] (running max in log2 units, sum)
+  unsigned* counters;      // arrival counters (in-kernel merge), else nullptr
   int B, N, H, L_cap, chunk, splits;
   float scale_log2;        // softmax scale * log2(e)
 };

@@ -37,8 +37,11 @@
 // 64-bit ancestor mask per query built by pointer doubling over the parents.
 //
 // The waves merge their (max, sum, O) states through LDS.  With more than one
-// split per (sequence, head) each workgroup writes a partial state and a
-// second small kernel merges the partials in a fixed split order.
+// split per (sequence, head) each workgroup writes a partial state, counts
+// itself in with one device-scope atomic, and the workgroup that completes
+// the (sequence, head) merges the partials in split order -- one launch per
+// call.  (Calls with more (sequence, head) pairs than counter slots leave
+// the merge to a second small kernel.)
 #include <hip/hip_runtime.h>
 #include <stdint.h>
 
@@ -434,6 +437,130 @@ __device__ __forceinline__ void store_2(uint16_t* dst, float a, float b) {
 
 __device__ __forceinline__ void store_2(float* dst, float a, float b) { *(float2*)dst = make_float2(a, b); }
 
+// Split partial states.  They are written and read with the device-scope
+// cache policy (sc1: stores written through past the XCD's L2, loads served
+// coherently), so the workgroup that merges a (sequence, head) sees the
+// states of every split whichever XCD -- and so whichever of the eight L2s --
+// wrote them: nothing depends on where the dispatcher places a workgroup.
+// One descriptor pair covers one (sequence, head): splits * N rows, at most
+// 64 * 64 * 512 bytes of outputs.
+constexpr int kDeviceScope = 16;  // sc1
+typedef __attribute__((ext_vector_type(2))) uint32_t u32x2_t;
+
+struct PartialRefs {
+  __amdgpu_buffer_rsrc_t o, ml;  // rows split * N + n: 128 floats / (max, sum)
+};
+
+__device__ __forceinline__ PartialRefs partial_refs(const AttnArgs& a, int b, int h) {
+  const int rows = a.splits * a.N;
+  const size_t first = ((size_t)b * a.H + h) * (size_t)rows;
+  PartialRefs r;
+  r.o = __builtin_amdgcn_make_buffer_rsrc(a.part_o + first * kD, (short)0, rows * kD * 4, kBufferDesc3);
+  r.ml = __builtin_amdgcn_make_buffer_rsrc(a.part_ml + first, (short)0, rows * 8, kBufferDesc3);
+  return r;
+}
+
+// `coherent`: device-scope stores for the in-kernel merge; the second-launch
+// merge reads the states after a kernel boundary and takes plain stores.
+template <int CPOL>
+__device__ __forceinline__ void store_partial_row8_p(const PartialRefs& p, int row, int d, const float (&o)[8]) {
+  const int off = (row * kD + d) * 4;
+  __builtin_amdgcn_raw_buffer_store_b128(__builtin_bit_cast(u32x4_t, f32x4_t{o[0], o[1], o[2], o[3]}), p.o,
+                                         off, 0, CPOL);
+  __builtin_amdgcn_raw_buffer_store_b128(__builtin_bit_cast(u32x4_t, f32x4_t{o[4], o[5], o[6], o[7]}), p.o,
+                                         off + 16, 0, CPOL);
+}
+
+__device__ __forceinline__ void store_partial_row8(const PartialRefs& p, int row, int d, const float (&o)[8],
+                                                   bool coherent) {
+  if (coherent)
+    store_partial_row8_p<kDeviceScope>(p, row, d, o);
+  else
+    store_partial_row8_p<0>(p, row, d, o);
+}
+
+__device__ __forceinline__ void store_partial_ml(const PartialRefs& p, int row, float m, float l,
+                                                 bool coherent) {
+  const u32x2_t v = __builtin_bit_cast(u32x2_t, f32x2_t{m, l});
+  if (coherent)
+    __builtin_amdgcn_raw_buffer_store_b64(v, p.ml, row * 8, 0, kDeviceScope);
+  else
+    __builtin_amdgcn_raw_buffer_store_b64(v, p.ml, row * 8, 0, 0);
+}
+
+// Called by every thread of a split's workgroup once its partial stores are
+// issued.  Each wave waits until its stores have completed at device scope;
+// then one thread counts the split in and publishes the answer in the LDS
+// word `flag` (a word the caller has free: the shared-step kernel passes one
+// inside its ring, whose 64 KB must not grow -- a byte more and only one
+// workgroup fits on a CU).  Returns true in the workgroup that completes the
+// (sequence, head) -- after resetting the counter for the next call -- and
+// false in the others, which are done.
+__device__ __forceinline__ bool last_to_arrive(unsigned* counter, int nsplit, int* flag) {
+  asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
+  __syncthreads();
+  if (threadIdx.x == 0) {
+    const unsigned before = __hip_atomic_fetch_add(counter, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    const bool last = before == (unsigned)(nsplit - 1);
+    if (last) __hip_atomic_store(counter, 0u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    *flag = last;
+  }
+  __syncthreads();
+  return *flag != 0;
+}
+
+// Merge of the split partial states of (sequence b, head h) by the
+// workgroup that finished last: thread t takes output row t / (128 / DPT)
+// and DPT head dims; the splits are combined in split order, so the result
+// does not depend on which workgroup merges.  (Rows of up to 2 * DPT
+// queries: DPT = 8 for 16 rows, 16 for 32, 32 for 64.)
+template <class P, int DPT>
+__device__ __forceinline__ void merge_partials(const AttnArgs& a, int b, int h, int nsplit) {
+  typedef typename P::elem_t elem_t;
+  constexpr int kTPR = kD / DPT;                          // threads per row
+  constexpr int kBatch = DPT == 8 ? 8 : (DPT == 16 ? 4 : 2);  // splits requested at once
+  const int tid = threadIdx.x;
+  const int n = tid / kTPR, d0 = DPT * (tid % kTPR);
+  if (n >= a.N) return;
+  const PartialRefs p = partial_refs(a, b, h);
+  float M = neg_inf(), L = 0.f, o[DPT];
+#pragma unroll
+  for (int e = 0; e < DPT; ++e) o[e] = 0.f;
+  for (int s0 = 0; s0 < nsplit; s0 += kBatch) {
+    f32x2_t ml[kBatch];
+    f32x4_t ov[kBatch][DPT / 4];
+#pragma unroll
+    for (int u = 0; u < kBatch; ++u) {
+      const int row = min(s0 + u, nsplit - 1) * a.N + n;
+      ml[u] = __builtin_bit_cast(f32x2_t, __builtin_amdgcn_raw_buffer_load_b64(p.ml, row * 8, 0, kDeviceScope));
+#pragma unroll
+      for (int q = 0; q < DPT / 4; ++q)
+        ov[u][q] = __builtin_bit_cast(
+            f32x4_t, __builtin_amdgcn_raw_buffer_load_b128(p.o, (row * kD + d0 + 4 * q) * 4, 0, kDeviceScope));
+    }
+#pragma unroll
+    for (int u = 0; u < kBatch; ++u) {
+      const bool valid = s0 + u < nsplit;
+      const float mu = valid ? ml[u][0] : neg_inf();
+      const float m_new = fmaxf(M, mu);
+      const float al = (m_new == neg_inf()) ? 0.f : fast_exp2(M - m_new);
+      const float f = (m_new == neg_inf()) ? 0.f : fast_exp2(mu - m_new);
+      L = L * al + (valid ? f * ml[u][1] : 0.f);
+#pragma unroll
+      for (int e = 0; e < DPT; ++e) o[e] = o[e] * al + (valid ? f * ov[u][e >> 2][e & 3] : 0.f);
+      M = m_new;
+    }
+  }
+  const float inv = (L > 0.f) ? 1.f / L : 0.f;
+  elem_t* dst = (elem_t*)a.out + (((size_t)b * a.N + n) * a.H + h) * kD + d0;
+#pragma unroll
+  for (int i = 0; i < DPT / 8; ++i) {
+    const float r[8] = {o[8 * i] * inv,     o[8 * i + 1] * inv, o[8 * i + 2] * inv, o[8 * i + 3] * inv,
+                        o[8 * i + 4] * inv, o[8 * i + 5] * inv, o[8 * i + 6] * inv, o[8 * i + 7] * inv};
+    store_row8(dst + 8 * i, r);
+  }
+}
+
 // Sequence taken by workgroup row y.  When every workgroup covers a whole
 // sequence (one split) and 2 <= B <= 64, the y-th longest (ties to the lower
 // index): the grid, dispatched in linear order, then starts the longest
@@ -599,7 +726,7 @@ void tree_attn_kernel(AttnArgs args) {
   }
   __syncthreads();
 
-  const size_t part_base = (((size_t)b * H + h) * args.splits + s) * N;
+  const PartialRefs pr = partial_refs(args, b, h);
 #pragma unroll
   for (int nt = 0; nt < NT; ++nt) {
     float mw[kWpg], fw[kWpg];
@@ -632,11 +759,15 @@ void tree_attn_kernel(AttnArgs args) {
         if (nsplit == 1)
           store_row8((elem_t*)args.out + (((size_t)b * N + n) * H + h) * kD + d, o);
         else
-          store_row8(args.part_o + (part_base + n) * kD + d, o);
+          store_partial_row8(pr, s * N + n, d, o, args.counters != nullptr);
       }
     }
-    if (nsplit > 1 && n < N && g == 0 && wig == 0) args.part_ml[part_base + n] = make_float2(M, L);
+    if (nsplit > 1 && n < N && g == 0 && wig == 0) store_partial_ml(pr, s * N + n, M, L, args.counters != nullptr);
   }
+  __shared__ int lds_last;
+  if (nsplit > 1 && args.counters &&
+      last_to_arrive(args.counters + ((size_t)b * H + h) * kCounterStride, nsplit, &lds_last))
+    merge_partials<P, 8 * NT * QG>(args, b, h, nsplit);
 }
 
 // ---------------------------------------------------------------------------
@@ -1145,12 +1276,19 @@ void block_attn_kernel(BlockAttnArgs args) {
 }
 
 template <class P, bool TREE>
-hipError_t launch_nt(const AttnArgs& a, hipStream_t stream) {
+hipError_t launch_nt(const AttnArgs& args, hipStream_t stream) {
   // Heads vary fastest and splits slowest: workgroups are handed to the XCDs
   // round-robin by linear id, so every split level spreads over all eight
   // XCDs, and the empty splits of short sequences sit at the end of the grid.
+  const int tiles = (args.N + 15) / 16;
+  // The in-kernel merge is taken by the register kernel only: on the
+  // shared-step kernel (bf16, 17..64 rows) it measured slower than the
+  // second launch (13B shape: 51.5 against 43.3 us per call), so that
+  // kernel leaves the counters alone and writes plain partial states.
+  const bool shared_step = std::is_same<P, Bf16Path>::value && tiles > 1;
+  AttnArgs a = args;
+  if (shared_step) a.counters = nullptr;
   const dim3 grid(a.H, a.B, a.splits), block(kThreads);
-  const int tiles = (a.N + 15) / 16;
   if (tiles == 1)
     hipLaunchKernelGGL((tree_attn_kernel<P, 1, 1, TREE>), grid, block, 0, stream, a);
   else if (std::is_same<P, Bf16Path>::value && tiles == 2)
@@ -1162,7 +1300,7 @@ hipError_t launch_nt(const AttnArgs& a, hipStream_t stream) {
   else
     hipLaunchKernelGGL((tree_attn_kernel<P, 2, 2, TREE>), grid, block, 0, stream, a);
   hipError_t e = hipGetLastError();
-  if (e != hipSuccess || a.splits == 1) return e;
+  if (e != hipSuccess || a.splits == 1 || a.counters) return e;
   const int rows = a.B * a.N * a.H;
   const dim3 cgrid((rows + kCombineRows - 1) / kCombineRows);
   if (a.splits <= 2)
@@ -1217,9 +1355,11 @@ AttnPlan plan_tree_attn(int B, int N, int H, int L_cap, int max_splits) {
     return p;
   }
   const size_t units = (size_t)bh * p.splits * N;
-  p.part_ml_off = 0;
-  p.part_o_off = (units * sizeof(float2) + 255) & ~(size_t)255;
+  p.counters_off = 0;
+  p.part_ml_off = kCounterBytes;
+  p.part_o_off = (p.part_ml_off + units * sizeof(float2) + 255) & ~(size_t)255;
   p.ws_bytes = p.part_o_off + units * kHeadDim * sizeof(float);
+  p.merge_in_kernel = bh <= kCounterSlots;
   return p;
 }
 

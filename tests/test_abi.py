@@ -111,6 +111,20 @@ def test_tree_attn_workspace_plan(lib):
     assert sizes == sorted(sizes)
 
 
+def test_tree_attn_workspace_layout(lib):
+    """A split workspace is the fixed 256 KiB counter block, then the (max,
+    sum) pair and the 128-float output of every (sequence, head, split,
+    query) row: the 7B verification layer's plan has 8 splits."""
+    assert glide.ATTN_COUNTER_BYTES == 256 << 10
+    units = 1 * 32 * 8 * 16
+    assert lib.glide_tree_attn_workspace(1, 16, 32, 128, 2064, 8) == (256 << 10) + units * 8 + units * 512
+    assert lib.glide_tree_attn_workspace(1, 16, 32, 128, 2064, 0) == (256 << 10) + units * 8 + units * 512
+    # the counter block does not grow with the number of (sequence, head) pairs
+    units = 33 * 64 * 3 * 5
+    ml = (units * 8 + 255) // 256 * 256
+    assert lib.glide_tree_attn_workspace(33, 5, 64, 128, 379, 3) == (256 << 10) + ml + units * 512
+
+
 def _cape(lib, **kw):
     a = dict(p=FAKE, B=1, gamma=5, V=32000, k=3, fixed=0, n_max=16, t=FAKE, par=FAKE, n=FAKE,
              ws=FAKE, ws_bytes=1 << 20)

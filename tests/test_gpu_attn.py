@@ -142,12 +142,15 @@ def test_deterministic_and_split_invariant():
 
 
 def test_workspace_reused_across_shapes():
-    """One workspace serves calls of different shapes in turn (each call
-    writes the partial states it reads)."""
+    """One workspace serves calls of different shapes in turn: each call
+    writes the partial states it reads (stale ones are garbage on purpose)
+    and leaves the arrival-counter block zero."""
     require_gpu()
     dev = torch.device("cuda")
     big = glide.attn_workspace(4, 64, 8, 4160, 0, dev)
-    ws = torch.full((big.numel(),), 0xFF, dtype=torch.uint8, device=dev)  # garbage on purpose
+    ws = torch.full((big.numel(),), 0xFF, dtype=torch.uint8, device=dev)  # stale partial states
+    cnt = ws[:glide.ATTN_COUNTER_BYTES]
+    cnt.zero_()  # the counter block starts zero (include/glide.h)
     shapes = [(4, 64, 8, 4096, 0), (1, 16, 2, 2048, 9), (2, 5, 3, 1000, 3), (4, 64, 8, 4096, 0),
               (1, 16, 2, 2048, 64)]
     for i, (B, N, H, L, splits) in enumerate(shapes):
@@ -162,6 +165,7 @@ def test_workspace_reused_across_shapes():
                               torch.tensor(lens, dtype=torch.int32, device=dev),
                               torch.from_numpy(par).to(dev), out, max_splits=splits, workspace=ws)
         torch.cuda.synchronize()
+        assert int(cnt.count_nonzero()) == 0
         got = to64(out)
         # sample two heads per shape against the oracle
         for b in range(B):
@@ -169,6 +173,65 @@ def test_workspace_reused_across_shapes():
                 ref = OA.tree_attention_head(to64(q[b, :, h]), to64(k[b, h]), to64(v[b, h]),
                                              lens[b], par[b])
                 assert float(np.abs(got[b, :, h] - ref).max()) <= BF16_TOL
+
+
+@pytest.mark.parametrize("tree", [True, False], ids=["tree", "cross"])
+def test_many_pairs_merge_in_second_launch(tree):
+    """More (sequence, head) pairs than arrival counters (B * H > 2048) with
+    several splits: the partial states are merged by the second launch;
+    sampled (sequence, head) pairs against the oracle, and a workspace whose
+    counter block stays zero."""
+    require_gpu()
+    dev = torch.device("cuda")
+    B, N, H = 33, 5, 64
+    lens = [150 + 7 * b for b in range(B)]
+    L_cap = max(lens) + N
+    say("many pairs", dict(B=B, N=N, H=H, tree=tree))
+    q = cpu_normal((B, N, H, D), 70, torch.bfloat16)
+    k = cpu_normal((B, H, L_cap, D), 71, torch.bfloat16)
+    v = cpu_normal((B, H, L_cap, D), 72, torch.bfloat16)
+    par = np.tile(np.arange(-1, N - 1, dtype=np.int32), (B, 1)) if tree else None
+    need = glide.load().glide_tree_attn_workspace(B, N, H, D, L_cap, 3)
+    ws = torch.zeros(need, dtype=torch.uint8, device=dev)
+    out = torch.full((B, N, H, D), float("nan"), dtype=torch.bfloat16, device=dev)
+    glide.glide_tree_attn(q.to(dev), k.to(dev), v.to(dev), torch.tensor(lens, dtype=torch.int32, device=dev),
+                          None if par is None else torch.from_numpy(par).to(dev), out, max_splits=3,
+                          workspace=ws)
+    torch.cuda.synchronize()
+    assert int(ws[:glide.ATTN_COUNTER_BYTES].count_nonzero()) == 0
+    got = to64(out)
+    assert np.isfinite(got).all()
+    for b in (0, 16, B - 1):
+        for h in (0, 31, H - 1):
+            ref = OA.tree_attention_head(to64(q[b, :, h]), to64(k[b, h]), to64(v[b, h]), lens[b],
+                                         None if par is None else par[b])
+            assert float(np.abs(got[b, :, h] - ref).max()) <= BF16_TOL
+
+
+def test_counter_block_left_zero():
+    """Every split call -- both kernels, both dtypes, tree and cross mode,
+    forced split counts up to 64 -- leaves the binding's cached workspace's
+    counter block zero, and a repeated call gives bit-identical results."""
+    require_gpu()
+    dev = torch.device("cuda")
+    for i, (B, N, H, L, dtype, splits, tree) in enumerate([
+            (1, 16, 32, 2048, torch.bfloat16, 0, True), (4, 32, 8, 1500, torch.bfloat16, 0, True),
+            (2, 64, 4, 3000, torch.bfloat16, 7, True), (3, 5, 16, 900, torch.bfloat16, 64, False),
+            (2, 40, 4, 1200, torch.float32, 5, True), (1, 16, 8, 600, torch.float32, 0, False)]):
+        say("counters", dict(B=B, N=N, H=H, L=L, dtype=str(dtype), splits=splits, tree=tree))
+        q = cpu_normal((B, N, H, D), 80 + i, dtype).to(dev)
+        k = cpu_normal((B, H, L + N, D), 90 + i, dtype).to(dev)
+        v = cpu_normal((B, H, L + N, D), 100 + i, dtype).to(dev)
+        lens = torch.tensor([L - 11 * b for b in range(B)], dtype=torch.int32, device=dev)
+        par = torch.from_numpy(W.random_parents(B, N, 6, i)).to(dev) if tree else None
+        outs = [torch.empty_like(q) for _ in range(2)]
+        for o in outs:
+            glide.glide_tree_attn(q, k, v, lens, par, o, max_splits=splits)
+        ws = glide.attn_workspace(B, N, H, L + N, splits, dev)
+        torch.cuda.synchronize()
+        assert ws is not None and int(ws[:glide.ATTN_COUNTER_BYTES].count_nonzero()) == 0
+        view = torch.int16 if dtype == torch.bfloat16 else torch.int32
+        assert torch.equal(outs[0].view(view), outs[1].view(view))
 
 
 def test_validation_reports_bad_device_data(monkeypatch):
