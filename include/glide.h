@@ -88,17 +88,17 @@ int glide_last_hip_error(void);
  * Workspace bytes glide_tree_attn needs for these sizes (0 when the call runs
  * without a workspace, i.e. with one split).  Arguments as glide_tree_attn.
  * The workspace starts with a fixed 256 KiB block of arrival counters (one per
- * (sequence, head), 128 bytes apart), followed by the per-split partial
- * softmax states (running max, running sum and unnormalised output of every
- * query row).  The workgroup of a split counts itself in once its states are
- * written, and the one that completes a (sequence, head) merges them, so a
- * call is a single launch.  The counter block must be zero before the
- * workspace's first use (zero-fill the whole buffer once); every call leaves
- * it zero, and the partial states need no initialisation, so one buffer of
- * the largest size needed can serve calls of any shape in turn.  It must not
- * be shared by calls that can run concurrently.  (Calls with B * H > 2048
- * merge in a second launch and do not use the counters.)  Returns 0 for
- * invalid sizes.
+ * head, 128 bytes apart), followed by the per-split partial softmax states
+ * (running max, running sum and unnormalised output of every query row).
+ * For a single sequence (B == 1, H <= 2048, 1..16 bf16 rows or any float32
+ * rows) the workgroup of a split counts itself in once its states are
+ * written, and the one that completes a head merges them, so the call is a
+ * single launch; other calls merge in a second launch and leave the counters
+ * alone.  The counter block must be zero before the workspace's first use
+ * (zero-fill the whole buffer once); every call leaves it zero, and the
+ * partial states need no initialisation, so one buffer of the largest size
+ * needed can serve calls of any shape in turn.  It must not be shared by
+ * calls that can run concurrently.  Returns 0 for invalid sizes.
  */
 size_t glide_tree_attn_workspace(int B, int N, int H, int D, int L_cap,
                                  int max_splits);

@@ -19,8 +19,8 @@ constexpr int kMinChunk = 128;     // smallest split the automatic plan makes
 // in a fixed block at offset 0 of every split workspace, so a buffer that
 // serves calls of different shapes never finds partial states where a later
 // call keeps counters.  The block must be zero before a workspace's first
-// use; every call leaves it zero.  Calls with more (sequence, head) pairs
-// than slots merge in a second launch instead.
+// use; every call leaves it zero.  Only single-sequence calls merge this
+// way (at most kCounterSlots heads); the others merge in a second launch.
 constexpr int kCounterSlots = 2048;
 constexpr int kCounterStride = 32;  // uint32 words: 128 bytes
 constexpr size_t kCounterBytes = (size_t)kCounterSlots * kCounterStride * 4;

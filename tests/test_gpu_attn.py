@@ -177,8 +177,9 @@ def test_workspace_reused_across_shapes():
 
 @pytest.mark.parametrize("tree", [True, False], ids=["tree", "cross"])
 def test_many_pairs_merge_in_second_launch(tree):
-    """More (sequence, head) pairs than arrival counters (B * H > 2048) with
-    several splits: the partial states are merged by the second launch;
+    """Many sequences (and more (sequence, head) pairs than arrival counters,
+    B * H > 2048) with several splits: the partial states are merged by the
+    second launch;
     sampled (sequence, head) pairs against the oracle, and a workspace whose
     counter block stays zero."""
     require_gpu()
