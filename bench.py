@@ -302,6 +302,18 @@ PROFILE_STEM = {"7b-1layer-chain5": "chain5", "vicuna7b-cape16": "vicuna7b",
                 "7b-longctx-cape64": "longctx"}
 
 
+def verify_kernels(wl):
+    """The launches one verification call of the workload makes, as the
+    library plans them (bf16)."""
+    ws = glide.load().glide_tree_attn_workspace(wl.batch, wl.nodes, wl.heads, wl.head_dim, wl.l_cap, 0)
+    main = "tree_attn_kernel" if wl.nodes <= 16 else "tree_attn_shared_kernel"
+    if ws == 0:
+        return main + ", one split per sequence"
+    if wl.batch == 1 and wl.nodes <= 16:
+        return main + ", split merge inside the kernel"
+    return main + " + tree_attn_combine"
+
+
 def load_traffic(wl_name="vicuna7b-cape16"):
     """HBM bytes per verification attention call of a workload from the
     committed rocprofv3 counter summary, or None when there is none or the
@@ -724,8 +736,7 @@ def main():
         "roofline": {"bound": "hbm", "achieved": round(achieved, 2), "peak": HBM_PEAK_GBPS,
                      "unit": "GB/s", "frac": round(achieved / HBM_PEAK_GBPS, 4),
                      "traffic": load_traffic(wl.name),
-                     "kernel": "glide_tree_attn call (tree_attn_kernel + tree_attn_combine), "
-                               "verification layer",
+                     "kernel": "glide_tree_attn call (%s), verification layer" % verify_kernels(wl),
                      "bytes_per_launch": step.verify_bytes,
                      "avg_launch_us": round(call_ms * 1e3, 3),
                      "timing": "HIP events around graph replays of the verification "
