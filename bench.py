@@ -290,10 +290,17 @@ def oracle_sampled(step, threads, budget_s=5.0):
 
 
 def kernel_source_hash():
+    """Hash of the attention kernels' code (comments and whitespace removed,
+    so that editing a comment does not orphan the counter summaries)."""
     import hashlib
-    src = b"".join(open(os.path.join(ROOT, "paper_2402_02082_amd", "csrc", n), "rb").read()
-                   for n in ("tree_attn.hip", "attn.h"))
-    return hashlib.sha256(src).hexdigest()[:16]
+    import re
+    code = []
+    for n in ("tree_attn.hip", "attn.h"):
+        text = open(os.path.join(ROOT, "paper_2402_02082_amd", "csrc", n)).read()
+        text = re.sub(r"/\*.*?\*/", " ", text, flags=re.S)
+        text = re.sub(r"//[^\n]*", " ", text)
+        code.append(" ".join(text.split()))
+    return hashlib.sha256("\n".join(code).encode()).hexdigest()[:16]
 
 
 # Stem of each workload's profile summaries under profiles/.

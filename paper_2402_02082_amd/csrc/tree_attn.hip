@@ -1282,9 +1282,10 @@ hipError_t launch_nt(const AttnArgs& args, hipStream_t stream) {
   // XCDs, and the empty splits of short sequences sit at the end of the grid.
   const int tiles = (args.N + 15) / 16;
   // The in-kernel merge is taken by the register kernel only: on the
-  // shared-step kernel (bf16, 17..64 rows) it measured slower than the
-  // second launch (13B shape: 51.5 against 43.3 us per call), so that
-  // kernel leaves the counters alone and writes plain partial states.
+  // shared-step kernel (bf16, 17..64 rows) the device-scope state stores
+  // slowed the streams still running (13B shape: 49.4 against 42.6 us per
+  // call), so that kernel leaves the counters alone and writes plain
+  // partial states.
   const bool shared_step = std::is_same<P, Bf16Path>::value && tiles > 1;
   AttnArgs a = args;
   if (shared_step) a.counters = nullptr;
