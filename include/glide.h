@@ -88,8 +88,12 @@ int glide_last_hip_error(void);
  * Workspace bytes glide_tree_attn needs for these sizes (0 when the call runs
  * without a workspace, i.e. with one split).  Arguments as glide_tree_attn.
  * The workspace starts with a fixed 256 KiB block of arrival counters (one per
- * head, 128 bytes apart), followed by the per-split partial softmax states
- * (running max, running sum and unnormalised output of every query row).
+ * head, 128 bytes apart, with the flags of the merge below), followed by the
+ * per-split partial softmax states (running max, running sum and the float32
+ * output of every query row) and, for a single sequence, the same rows in
+ * fp16: single-sequence bf16 calls exchange each split's normalised output
+ * in fp16, and in float32 only for the pieces whose values exceed fp16's
+ * range.
  * For a single sequence (B == 1, H <= 2048, 1..16 bf16 rows or any float32
  * rows) the workgroup of a split counts itself in once its states are
  * written, and the one that completes a head merges them, so the call is a
@@ -133,6 +137,11 @@ size_t glide_tree_attn_workspace(int B, int N, int H, int D, int L_cap,
  *   max_splits   0 = choose automatically, else 1..64 key-range splits.
  *   workspace    device buffer of >= glide_tree_attn_workspace(...) bytes;
  *                may be NULL when that size is 0.
+ * Precision: scores, softmax sums and outputs accumulate in float32; with
+ * bf16 inputs the probabilities enter the PV product rounded to bf16, and
+ * a single-sequence call with several splits exchanges each split's
+ * normalised output in fp16 (at most 2^-11 of its size off; float32 when
+ * out of fp16's range).  The output is rounded to dtype once.
  */
 int glide_tree_attn(const void* q, const void* k_cache, const void* v_cache,
                     const int32_t* seq_lens, const int32_t* tree_parents,

@@ -24,13 +24,16 @@ constexpr int kMinChunk = 128;     // smallest split the automatic plan makes
 constexpr int kCounterSlots = 2048;
 constexpr int kCounterStride = 32;  // uint32 words: 128 bytes
 constexpr size_t kCounterBytes = (size_t)kCounterSlots * kCounterStride * 4;
+// Words 1..8 of a head's counter slot flag the (split, wave) pieces whose
+// states did not fit fp16 (bit 4 * split + wave; up to 64 splits).
+constexpr int kWideFlagWords = 8;
 
 // How the keys of one (sequence, head) are divided between workgroups.
 struct AttnPlan {
   int splits;       // workgroups per (sequence, head)
   int chunk;        // keys per workgroup (multiple of kChunkQuantum)
   size_t ws_bytes;  // workspace: counters + partial states (0 if splits == 1)
-  size_t counters_off, part_o_off, part_ml_off;
+  size_t counters_off, part_o_off, part_ml_off, part_h_off;
   bool merge_in_kernel;  // the last split to finish merges (else a second launch)
 };
 
@@ -45,6 +48,7 @@ struct AttnArgs {
   void* out;
   float* part_o;           // [B, H, splits, N, D]
   float2* part_ml;         // [B, H, splits, N] (running max in log2 units, sum)
+  uint16_t* part_h;        // [B, H, splits, N, D] fp16 (in-kernel merge of bf16 calls)
   unsigned* counters;      // arrival counters (in-kernel merge), else nullptr
   int B, N, H, L_cap, chunk, splits;
   float scale_log2;        // softmax scale * log2(e)

@@ -488,6 +488,39 @@ __device__ __forceinline__ void store_partial_ml(const PartialRefs& p, int row, 
     __builtin_amdgcn_raw_buffer_store_b64(v, p.ml, row * 8, 0, 0);
 }
 
+// fp16 split states (bf16 inputs, in-kernel merge): the normalised output
+// o / L of a query row in half precision, rounded to nearest even (one
+// conversion per pair): a value's error is at most 2^-11 of its size, a
+// quarter of what the bf16 rounding of every probability already allows.
+// Rows of a wave that holds a value fp16 cannot represent (|x| > 65504,
+// infinities, NaN) are also written in float32 to the float32 state rows,
+// and the wave sets its (split, wave) bit in the flag words of the head's
+// counter slot; the merge reads those rows instead.
+constexpr float kHalfMax = 65504.f;
+typedef __attribute__((ext_vector_type(2))) _Float16 f16x2_t;
+
+__device__ __forceinline__ uint32_t pack_f16x2(float lo, float hi) {
+  return __builtin_bit_cast(uint32_t, __builtin_convertvector((f32x2_t{lo, hi}), f16x2_t));
+}
+
+__device__ __forceinline__ float2 unpack_f16x2(uint32_t w) {
+  const f16x2_t h = __builtin_bit_cast(f16x2_t, w);
+  const f32x2_t f = __builtin_convertvector(h, f32x2_t);
+  return make_float2(f[0], f[1]);
+}
+
+// fp16 rows: one descriptor per (sequence, head), splits * N rows of 256 B.
+__device__ __forceinline__ __amdgpu_buffer_rsrc_t half_refs(const AttnArgs& a, int b, int h) {
+  const int rows = a.splits * a.N;
+  const size_t first = ((size_t)b * a.H + h) * (size_t)rows;
+  return __builtin_amdgcn_make_buffer_rsrc(a.part_h + first * kD, (short)0, rows * kD * 2, kBufferDesc3);
+}
+
+__device__ __forceinline__ void store_half_row8(__amdgpu_buffer_rsrc_t r, int row, int d, const float (&o)[8]) {
+  const u32x4_t w = {pack_f16x2(o[0], o[1]), pack_f16x2(o[2], o[3]), pack_f16x2(o[4], o[5]), pack_f16x2(o[6], o[7])};
+  __builtin_amdgcn_raw_buffer_store_b128(w, r, (row * kD + d) * 2, 0, kDeviceScope);
+}
+
 // Called by every thread of a split's workgroup once its partial stores are
 // issued.  Each wave waits until its stores have completed at device scope;
 // then one thread counts the split in and publishes the answer in the LDS
@@ -514,50 +547,105 @@ __device__ __forceinline__ bool last_to_arrive(unsigned* counter, int nsplit, in
 // and DPT head dims; the splits are combined in split order, so the result
 // does not depend on which workgroup merges.  (Rows of up to 2 * DPT
 // queries: DPT = 8 for 16 rows, 16 for 32, 32 for 64.)
+// States from float32 inputs are the unnormalised (max, sum, O) of the
+// second-launch merge.  States from bf16 inputs hold o / L: fp16 rows,
+// requested together with every split's (max, sum) and the head's flag
+// words, then -- for the (split, wave) pieces flagged there -- float32 rows
+// in a second round.  Each split then enters with weight 2^(m_s - M) L_s.
+// The merging workgroup clears the flags it found set.
 template <class P, int DPT>
 __device__ __forceinline__ void merge_partials(const AttnArgs& a, int b, int h, int nsplit) {
   typedef typename P::elem_t elem_t;
+  constexpr bool kHalf = std::is_same<P, Bf16Path>::value && DPT == 8;
   constexpr int kTPR = kD / DPT;                          // threads per row
   constexpr int kBatch = DPT == 8 ? 8 : (DPT == 16 ? 4 : 2);  // splits requested at once
   const int tid = threadIdx.x;
   const int n = tid / kTPR, d0 = DPT * (tid % kTPR);
-  if (n >= a.N) return;
   const PartialRefs p = partial_refs(a, b, h);
-  float M = neg_inf(), L = 0.f, o[DPT];
+  // fp16 rows, and the head's flag words: a batch of 8 splits is one word
+  // (bit 4 u + wave), so word s0 / 8 comes with the batch's requests.
+  const __amdgpu_buffer_rsrc_t ph = kHalf ? half_refs(a, b, h) : p.o;
+  const __amdgpu_buffer_rsrc_t pf = __builtin_amdgcn_make_buffer_rsrc(
+      a.counters + ((size_t)b * a.H + h) * kCounterStride + 1, (short)0, kWideFlagWords * 4, kBufferDesc3);
+  const int r = (d0 & 31) >> 3;  // the wave of the split that wrote these dims
+  uint32_t flagged = 0;  // batches whose flag word was set (thread 0 clears them)
+  if (n < a.N) {
+    float M = neg_inf(), L = 0.f, o[DPT];
 #pragma unroll
-  for (int e = 0; e < DPT; ++e) o[e] = 0.f;
-  for (int s0 = 0; s0 < nsplit; s0 += kBatch) {
-    f32x2_t ml[kBatch];
-    f32x4_t ov[kBatch][DPT / 4];
+    for (int e = 0; e < DPT; ++e) o[e] = 0.f;
+    for (int s0 = 0; s0 < nsplit; s0 += kBatch) {
+      f32x2_t ml[kBatch];
+      float x[kBatch][DPT];
+      const uint32_t wide = kHalf ? __builtin_amdgcn_raw_buffer_load_b32(pf, (s0 / 8) * 4, 0, kDeviceScope) : 0u;
 #pragma unroll
-    for (int u = 0; u < kBatch; ++u) {
-      const int row = min(s0 + u, nsplit - 1) * a.N + n;
-      ml[u] = __builtin_bit_cast(f32x2_t, __builtin_amdgcn_raw_buffer_load_b64(p.ml, row * 8, 0, kDeviceScope));
+      for (int u = 0; u < kBatch; ++u) {
+        const int row = min(s0 + u, nsplit - 1) * a.N + n;
+        ml[u] = __builtin_bit_cast(f32x2_t, __builtin_amdgcn_raw_buffer_load_b64(p.ml, row * 8, 0, kDeviceScope));
+        if (kHalf) {
+          const u32x4_t hv = __builtin_bit_cast(
+              u32x4_t, __builtin_amdgcn_raw_buffer_load_b128(ph, (row * kD + d0) * 2, 0, kDeviceScope));
 #pragma unroll
-      for (int q = 0; q < DPT / 4; ++q)
-        ov[u][q] = __builtin_bit_cast(
-            f32x4_t, __builtin_amdgcn_raw_buffer_load_b128(p.o, (row * kD + d0 + 4 * q) * 4, 0, kDeviceScope));
+          for (int w = 0; w < 4; ++w) {
+            const float2 f = unpack_f16x2(hv[w]);
+            x[u][2 * w] = f.x;
+            x[u][2 * w + 1] = f.y;
+          }
+        } else {
+#pragma unroll
+          for (int q = 0; q < DPT / 4; ++q) {
+            const f32x4_t v = __builtin_bit_cast(
+                f32x4_t, __builtin_amdgcn_raw_buffer_load_b128(p.o, (row * kD + d0 + 4 * q) * 4, 0, kDeviceScope));
+#pragma unroll
+            for (int e = 0; e < 4; ++e) x[u][4 * q + e] = v[e];
+          }
+        }
+      }
+      if (kHalf && wide != 0u) {  // rare: float32 rows of the flagged pieces
+#pragma unroll
+        for (int u = 0; u < kBatch; ++u) {
+          if (s0 + u < nsplit && ((wide >> (4 * u + r)) & 1u)) {
+            const int row = (s0 + u) * a.N + n;
+#pragma unroll
+            for (int q = 0; q < 2; ++q) {
+              const f32x4_t v = __builtin_bit_cast(
+                  f32x4_t, __builtin_amdgcn_raw_buffer_load_b128(p.o, (row * kD + d0 + 4 * q) * 4, 0, kDeviceScope));
+#pragma unroll
+              for (int e = 0; e < 4; ++e) x[u][4 * q + e] = v[e];
+            }
+          }
+        }
+        flagged |= 1u << (s0 / 8);
+      }
+#pragma unroll
+      for (int u = 0; u < kBatch; ++u) {
+        const bool valid = s0 + u < nsplit;
+        const float mu = valid ? ml[u][0] : neg_inf();
+        const float m_new = fmaxf(M, mu);
+        const float al = (m_new == neg_inf()) ? 0.f : fast_exp2(M - m_new);
+        const float f = (m_new == neg_inf()) ? 0.f : fast_exp2(mu - m_new);
+        const float w = kHalf ? f * ml[u][1] : f;  // fp16 rows are normalised
+        L = L * al + (valid ? f * ml[u][1] : 0.f);
+#pragma unroll
+        for (int e = 0; e < DPT; ++e) o[e] = o[e] * al + (valid ? w * x[u][e] : 0.f);
+        M = m_new;
+      }
     }
+    const float inv = (L > 0.f) ? 1.f / L : 0.f;
+    elem_t* dst = (elem_t*)a.out + (((size_t)b * a.N + n) * a.H + h) * kD + d0;
 #pragma unroll
-    for (int u = 0; u < kBatch; ++u) {
-      const bool valid = s0 + u < nsplit;
-      const float mu = valid ? ml[u][0] : neg_inf();
-      const float m_new = fmaxf(M, mu);
-      const float al = (m_new == neg_inf()) ? 0.f : fast_exp2(M - m_new);
-      const float f = (m_new == neg_inf()) ? 0.f : fast_exp2(mu - m_new);
-      L = L * al + (valid ? f * ml[u][1] : 0.f);
-#pragma unroll
-      for (int e = 0; e < DPT; ++e) o[e] = o[e] * al + (valid ? f * ov[u][e >> 2][e & 3] : 0.f);
-      M = m_new;
+    for (int i = 0; i < DPT / 8; ++i) {
+      const float rr[8] = {o[8 * i] * inv,     o[8 * i + 1] * inv, o[8 * i + 2] * inv, o[8 * i + 3] * inv,
+                           o[8 * i + 4] * inv, o[8 * i + 5] * inv, o[8 * i + 6] * inv, o[8 * i + 7] * inv};
+      store_row8(dst + 8 * i, rr);
     }
   }
-  const float inv = (L > 0.f) ? 1.f / L : 0.f;
-  elem_t* dst = (elem_t*)a.out + (((size_t)b * a.N + n) * a.H + h) * kD + d0;
-#pragma unroll
-  for (int i = 0; i < DPT / 8; ++i) {
-    const float r[8] = {o[8 * i] * inv,     o[8 * i + 1] * inv, o[8 * i + 2] * inv, o[8 * i + 3] * inv,
-                        o[8 * i + 4] * inv, o[8 * i + 5] * inv, o[8 * i + 6] * inv, o[8 * i + 7] * inv};
-    store_row8(dst + 8 * i, r);
+  if (kHalf) {
+    // every thread has read the flags; thread 0 (row 0, which every batch
+    // passes through) clears the words it found set, for the next call
+    __syncthreads();
+    if (tid == 0)
+      for (int k = 0; k < kWideFlagWords; ++k)
+        if ((flagged >> k) & 1u) __builtin_amdgcn_raw_buffer_store_b32(0u, pf, k * 4, 0, kDeviceScope);
   }
 }
 
@@ -724,6 +812,10 @@ void tree_attn_kernel(AttnArgs args) {
       lds_o[qg][wig][nt][r][1][lane] = f32x4_t{acc[nt][4][r], acc[nt][5][r], acc[nt][6][r], acc[nt][7][r]};
     }
   }
+  // Split states merged inside the kernel (single sequence) from bf16
+  // inputs are stored as o / L in fp16 (see store_half_row8).
+  constexpr bool kHalfCapable = std::is_same<P, Bf16Path>::value && NT == 1 && QG == 1;
+  const bool half_states = kHalfCapable && nsplit > 1 && args.counters != nullptr;
   __syncthreads();
 
   const PartialRefs pr = partial_refs(args, b, h);
@@ -742,7 +834,7 @@ void tree_attn_kernel(AttnArgs args) {
     for (int w = 1; w < kWpg; ++w) L += fw[w] * lds_l[qg][w][nt][lane];
 
     const int n = 16 * (qg * NT + nt) + c;
-    const float inv = (nsplit == 1) ? ((L > 0.f) ? 1.f / L : 0.f) : 1.f;
+    const float inv = (nsplit == 1 || half_states) ? ((L > 0.f) ? 1.f / L : 0.f) : 1.f;
 #pragma unroll
     for (int i = 0; i < kRPerWave; ++i) {
       const int r = wig * kRPerWave + i;
@@ -754,8 +846,21 @@ void tree_attn_kernel(AttnArgs args) {
       }
       const float o[8] = {lo4[0] * inv, lo4[1] * inv, lo4[2] * inv, lo4[3] * inv,
                           hi4[0] * inv, hi4[1] * inv, hi4[2] * inv, hi4[3] * inv};
-      if (n < N) {
-        const int d = 32 * g + 8 * r;
+      const int d = 32 * g + 8 * r;
+      if (half_states) {
+        bool fits = true;
+#pragma unroll
+        for (int e = 0; e < 8; ++e) fits &= __builtin_fabsf(o[e]) <= kHalfMax;  // false for NaN too
+        if (n < N) store_half_row8(half_refs(args, b, h), s * N + n, d, o);
+        if (!__all(fits || n >= N)) {  // wave-uniform: rare
+          if (n < N) store_partial_row8(pr, s * N + n, d, o, true);
+          if (lane == 0) {
+            const int bit = 4 * s + r;
+            __hip_atomic_fetch_or(args.counters + ((size_t)b * H + h) * kCounterStride + 1 + (bit >> 5),
+                                  1u << (bit & 31), __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+          }
+        }
+      } else if (n < N) {
         if (nsplit == 1)
           store_row8((elem_t*)args.out + (((size_t)b * N + n) * H + h) * kD + d, o);
         else
@@ -1367,6 +1472,10 @@ AttnPlan plan_tree_attn(int B, int N, int H, int L_cap, int max_splits) {
   // batch of four, 16 rows: 62.3 against 59.8 us per call with the second
   // launch; two equal sequences: 19.4 against 18.0 us).
   p.merge_in_kernel = B == 1 && bh <= kCounterSlots;
+  if (p.merge_in_kernel) {  // fp16 states of bf16 calls
+    p.part_h_off = (p.ws_bytes + 255) & ~(size_t)255;
+    p.ws_bytes = p.part_h_off + units * kHeadDim * sizeof(uint16_t);
+  }
   return p;
 }
 

@@ -114,11 +114,14 @@ def test_tree_attn_workspace_plan(lib):
 def test_tree_attn_workspace_layout(lib):
     """A split workspace is the fixed 256 KiB counter block, then the (max,
     sum) pair and the 128-float output of every (sequence, head, split,
-    query) row: the 7B verification layer's plan has 8 splits."""
+    query) row, and -- single-sequence calls, whose splits merge inside the
+    kernel -- the 128 fp16 values of every row: the 7B verification layer's
+    plan has 8 splits."""
     assert glide.ATTN_COUNTER_BYTES == 256 << 10
     units = 1 * 32 * 8 * 16
-    assert lib.glide_tree_attn_workspace(1, 16, 32, 128, 2064, 8) == (256 << 10) + units * 8 + units * 512
-    assert lib.glide_tree_attn_workspace(1, 16, 32, 128, 2064, 0) == (256 << 10) + units * 8 + units * 512
+    want = (256 << 10) + units * 8 + units * 512 + units * 256
+    assert lib.glide_tree_attn_workspace(1, 16, 32, 128, 2064, 8) == want
+    assert lib.glide_tree_attn_workspace(1, 16, 32, 128, 2064, 0) == want
     # the counter block does not grow with the number of (sequence, head) pairs
     units = 33 * 64 * 3 * 5
     ml = (units * 8 + 255) // 256 * 256

@@ -320,3 +320,82 @@ def test_largest_float32_cache(splits):
     del q, k, v
     torch.cuda.empty_cache()
     assert np.all(got == 2.0), got.ravel()[:4]
+
+
+def _single_and_pair(q, k, v, L, par, splits):
+    """The same sequence run alone (B = 1: split states merged inside the
+    kernel, fp16 o / L from bf16 inputs) and as sequence 0 of a pair whose
+    second sequence is empty (B = 2: float32 states merged by the second
+    launch), with the same forced split plan."""
+    dev = torch.device("cuda")
+    N, H = q.shape[1], q.shape[2]
+    one = torch.full_like(q, float("nan"))
+    glide.glide_tree_attn(q, k, v, torch.tensor([L], dtype=torch.int32, device=dev), par, one,
+                          max_splits=splits)
+    q2 = torch.cat([q, q]).contiguous()
+    k2, v2 = torch.cat([k, k]).contiguous(), torch.cat([v, v]).contiguous()
+    par2 = None if par is None else torch.cat([par, par]).contiguous()
+    two = torch.full((2, N, H, D), float("nan"), dtype=q.dtype, device=dev)
+    glide.glide_tree_attn(q2, k2, v2, torch.tensor([L, 0], dtype=torch.int32, device=dev), par2, two,
+                          max_splits=splits)
+    torch.cuda.synchronize()
+    return to64(one[0]), to64(two[0])
+
+
+@pytest.mark.parametrize("tree", [True, False], ids=["tree", "cross"])
+def test_half_states_match_float32_states(tree):
+    """Single-sequence bf16 calls keep each split's normalised output o / L
+    in fp16 (rounded to nearest even: error at most 2^-11 of the value, and
+    the merge is a convex combination of the splits' values); against the
+    float32 states of the two-launch merge on the same splits the outputs
+    differ by at most 2^-11 max |v| plus one bf16 ulp (each side rounded
+    once: up to 2^-7 of the value apart).  Both are within the oracle's
+    bound."""
+    require_gpu()
+    dev = torch.device("cuda")
+    N, H, L = (16 if tree else 5), 8, 2048
+    for splits in (8, 3):
+        say("half states", dict(tree=tree, splits=splits))
+        q = cpu_normal((1, N, H, D), 61, torch.bfloat16).to(dev)
+        k = cpu_normal((1, H, L + N, D), 62, torch.bfloat16).to(dev)
+        v = cpu_normal((1, H, L + N, D), 63, torch.bfloat16).to(dev)
+        par = torch.from_numpy(_parents("cape", 1, N, 64)).to(dev) if tree else None
+        one, two = _single_and_pair(q, k, v, L, par, splits)
+        vmax = float(to64(v).__abs__().max())
+        bound = 2.0 ** -11 * vmax + 2.0 ** -7 * np.maximum(np.abs(one), np.abs(two)) + 1e-6
+        assert float((np.abs(one - two) - bound).max()) <= 0
+        ref = OA.tree_attention(to64(q), to64(k), to64(v), [L], None if par is None else par.cpu().numpy())[0]
+        assert float(np.abs(one - ref).max()) <= BF16_TOL
+
+
+@pytest.mark.parametrize("where", ["one split", "every split"])
+def test_half_states_fall_back_to_float32(where):
+    """Value rows near 2e5 (representable in bf16, beyond fp16's 65504):
+    every split whose normalised output does not fit fp16 stores float32
+    rows instead (its sum stored negated).  Large rows inside one split only
+    (the others keep fp16 states of N(0, 1) rows) or in every split; the
+    result is finite and matches the float32-state merge within one bf16
+    ulp plus 2^-11 of the fp16 splits' values, and the oracle, scaled."""
+    require_gpu()
+    dev = torch.device("cuda")
+    N, H, L, splits = 16, 4, 2048, 8
+    big = 2.0e5
+    say("half states fallback", dict(where=where))
+    q = cpu_normal((1, N, H, D), 71, torch.bfloat16)
+    k = cpu_normal((1, H, L + N, D), 72, torch.bfloat16)
+    v = cpu_normal((1, H, L + N, D), 73, torch.float32)
+    rows = slice(300, 560) if where == "one split" else slice(0, L + N)  # keys 288..575: split 1
+    small = float(torch.cat([v[:, :, :300], v[:, :, 560:]], dim=2).abs().max()) if where == "one split" else 0.0
+    v[:, :, rows] = big * (1.0 + 0.01 * v[:, :, rows])
+    v = v.to(torch.bfloat16)
+    q, k, v = q.to(dev), k.to(dev), v.to(dev)
+    par = torch.from_numpy(_parents("cape", 1, N, 74)).to(dev)
+    one, two = _single_and_pair(q, k, v, L, par, splits)
+    # split 1's states are ~2e5 either way (they would overflow fp16 to
+    # infinities); with every row large so are the outputs
+    assert np.isfinite(one).all()
+    assert np.abs(one).max() > (65504 if where == "every split" else 1.0e4)
+    bound = 2.0 ** -11 * small + 2.0 ** -7 * np.maximum(np.abs(one), np.abs(two)) + 1e-6 * big
+    assert float((np.abs(one - two) - bound).max()) <= 0
+    ref = OA.tree_attention(to64(q), to64(k), to64(v), [L], par.cpu().numpy())[0]
+    assert float((np.abs(one - ref) - (BF16_TOL * big + 2.0 ** -8 * np.abs(ref))).max()) <= 0
