@@ -90,8 +90,8 @@ int glide_last_hip_error(void);
  * The workspace starts with a fixed 256 KiB block of arrival counters (one per
  * head, 128 bytes apart, with the flags of the merge below), followed by the
  * per-split partial softmax states (running max, running sum and the float32
- * output of every query row) and, for a single sequence, the same rows in
- * fp16: single-sequence bf16 calls exchange each split's normalised output
+ * output of every query row) and, for a single sequence of N >= 8 rows, the
+ * same rows in fp16: such bf16 calls exchange each split's normalised output
  * in fp16, and in float32 only for the pieces whose values exceed fp16's
  * range.
  * For a single sequence (B == 1, H <= 2048, 1..16 bf16 rows or any float32
@@ -139,9 +139,9 @@ size_t glide_tree_attn_workspace(int B, int N, int H, int D, int L_cap,
  *                may be NULL when that size is 0.
  * Precision: scores, softmax sums and outputs accumulate in float32; with
  * bf16 inputs the probabilities enter the PV product rounded to bf16, and
- * a single-sequence call with several splits exchanges each split's
- * normalised output in fp16 (at most 2^-11 of its size off; float32 when
- * out of fp16's range).  The output is rounded to dtype once.
+ * a single-sequence call of 8 or more rows with several splits exchanges
+ * each split's normalised output in fp16 (at most 2^-11 of its size off;
+ * float32 when out of fp16's range).  The output is rounded to dtype once.
  */
 int glide_tree_attn(const void* q, const void* k_cache, const void* v_cache,
                     const int32_t* seq_lens, const int32_t* tree_parents,

@@ -83,7 +83,7 @@ glide::AttnArgs attn_args(const void* q, const void* k_cache, const void* v_cach
   a.part_o = plan.ws_bytes ? (float*)(ws + plan.part_o_off) : nullptr;
   a.part_ml = plan.ws_bytes ? (float2*)(ws + plan.part_ml_off) : nullptr;
   a.counters = plan.ws_bytes && plan.merge_in_kernel ? (unsigned*)(ws + plan.counters_off) : nullptr;
-  a.part_h = plan.ws_bytes && plan.merge_in_kernel ? (uint16_t*)(ws + plan.part_h_off) : nullptr;
+  a.part_h = plan.ws_bytes && plan.half_states ? (uint16_t*)(ws + plan.part_h_off) : nullptr;
   a.B = B;
   a.N = N;
   a.H = H;

@@ -35,6 +35,7 @@ struct AttnPlan {
   size_t ws_bytes;  // workspace: counters + partial states (0 if splits == 1)
   size_t counters_off, part_o_off, part_ml_off, part_h_off;
   bool merge_in_kernel;  // the last split to finish merges (else a second launch)
+  bool half_states;      // bf16 states exchanged as fp16 o / L (in-kernel merge, N >= 8)
 };
 
 AttnPlan plan_tree_attn(int B, int N, int H, int L_cap, int max_splits);

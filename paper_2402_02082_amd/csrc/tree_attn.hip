@@ -553,10 +553,10 @@ __device__ __forceinline__ bool last_to_arrive(unsigned* counter, int nsplit, in
 // words, then -- for the (split, wave) pieces flagged there -- float32 rows
 // in a second round.  Each split then enters with weight 2^(m_s - M) L_s.
 // The merging workgroup clears the flags it found set.
-template <class P, int DPT>
+template <class P, int DPT, bool HALF>
 __device__ __forceinline__ void merge_partials(const AttnArgs& a, int b, int h, int nsplit) {
   typedef typename P::elem_t elem_t;
-  constexpr bool kHalf = std::is_same<P, Bf16Path>::value && DPT == 8;
+  constexpr bool kHalf = HALF && std::is_same<P, Bf16Path>::value && DPT == 8;
   constexpr int kTPR = kD / DPT;                          // threads per row
   constexpr int kBatch = DPT == 8 ? 8 : (DPT == 16 ? 4 : 2);  // splits requested at once
   const int tid = threadIdx.x;
@@ -815,7 +815,7 @@ void tree_attn_kernel(AttnArgs args) {
   // Split states merged inside the kernel (single sequence) from bf16
   // inputs are stored as o / L in fp16 (see store_half_row8).
   constexpr bool kHalfCapable = std::is_same<P, Bf16Path>::value && NT == 1 && QG == 1;
-  const bool half_states = kHalfCapable && nsplit > 1 && args.counters != nullptr;
+  const bool half_states = kHalfCapable && nsplit > 1 && args.counters != nullptr && args.part_h != nullptr;
   __syncthreads();
 
   const PartialRefs pr = partial_refs(args, b, h);
@@ -871,8 +871,12 @@ void tree_attn_kernel(AttnArgs args) {
   }
   __shared__ int lds_last;
   if (nsplit > 1 && args.counters &&
-      last_to_arrive(args.counters + ((size_t)b * H + h) * kCounterStride, nsplit, &lds_last))
-    merge_partials<P, 8 * NT * QG>(args, b, h, nsplit);
+      last_to_arrive(args.counters + ((size_t)b * H + h) * kCounterStride, nsplit, &lds_last)) {
+    if (half_states)
+      merge_partials<P, 8 * NT * QG, true>(args, b, h, nsplit);
+    else
+      merge_partials<P, 8 * NT * QG, false>(args, b, h, nsplit);
+  }
 }
 
 // ---------------------------------------------------------------------------
@@ -1472,7 +1476,11 @@ AttnPlan plan_tree_attn(int B, int N, int H, int L_cap, int max_splits) {
   // batch of four, 16 rows: 62.3 against 59.8 us per call with the second
   // launch; two equal sequences: 19.4 against 18.0 us).
   p.merge_in_kernel = B == 1 && bh <= kCounterSlots;
-  if (p.merge_in_kernel) {  // fp16 states of bf16 calls
+  // fp16 states (bf16 calls) pay from 8 query rows on: one 16-node layer
+  // 13.0 -> 11.8 us, an 8-node one 11.8 -> 11.4 us; 5 rows gain nothing
+  // (5-query cross layer) or lose (5-chain over 512 keys: 7.6 -> 8.0 us).
+  p.half_states = p.merge_in_kernel && N >= 8;
+  if (p.half_states) {
     p.part_h_off = (p.ws_bytes + 255) & ~(size_t)255;
     p.ws_bytes = p.part_h_off + units * kHeadDim * sizeof(uint16_t);
   }
