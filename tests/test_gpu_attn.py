@@ -399,3 +399,33 @@ def test_half_states_fall_back_to_float32(where):
     assert float((np.abs(one - two) - bound).max()) <= 0
     ref = OA.tree_attention(to64(q), to64(k), to64(v), [L], par.cpu().numpy())[0]
     assert float((np.abs(one - ref) - (BF16_TOL * big + 2.0 ** -8 * np.abs(ref))).max()) <= 0
+
+
+def test_half_states_flags_across_batches():
+    """64 splits (eight merge batches of eight, one flag word each): value
+    rows near 2e5 in splits 5, 37 and 63 only, so flag words 0, 4 and 7
+    carry bits and the others none; two calls in a row (the merge clears
+    the words it found set).  Against the float32-state merge within one
+    bf16 ulp plus 2^-11 of the fp16 splits' values, and against the oracle."""
+    require_gpu()
+    dev = torch.device("cuda")
+    N, H, L, splits = 16, 2, 64 * 128 - 16, 64
+    big = 2.0e5
+    say("half states flags", dict(N=N, H=H, L=L, splits=splits))
+    q = cpu_normal((1, N, H, D), 81, torch.bfloat16)
+    k = cpu_normal((1, H, L + N, D), 82, torch.bfloat16)
+    v = cpu_normal((1, H, L + N, D), 83, torch.float32)
+    small = float(v.abs().max())
+    for sp in (5, 37, 63):  # splits of 128 keys
+        v[:, :, 128 * sp + 10:128 * sp + 100] = big * (1.0 + 0.01 * v[:, :, 128 * sp + 10:128 * sp + 100])
+    v = v.to(torch.bfloat16)
+    q, k, v = q.to(dev), k.to(dev), v.to(dev)
+    par = torch.from_numpy(_parents("cape", 1, N, 84)).to(dev)
+    first, two = _single_and_pair(q, k, v, L, par, splits)
+    again, _ = _single_and_pair(q, k, v, L, par, splits)
+    assert np.array_equal(first, again)
+    assert np.isfinite(first).all()
+    bound = 2.0 ** -11 * small + 2.0 ** -7 * np.maximum(np.abs(first), np.abs(two)) + 1e-6 * big
+    assert float((np.abs(first - two) - bound).max()) <= 0
+    ref = OA.tree_attention(to64(q), to64(k), to64(v), [L], par.cpu().numpy())[0]
+    assert float((np.abs(first - ref) - (BF16_TOL * big + 2.0 ** -8 * np.abs(ref))).max()) <= 0
