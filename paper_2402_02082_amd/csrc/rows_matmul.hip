@@ -13,7 +13,8 @@
 // same operand shapes as the attention kernel's K * Q^T.  Loads go through
 // range-checked buffer descriptors (weight rows past N and activation rows
 // past M read as zeros), five to eight steps in flight per wave in
-// registers.
+// registers.  From three activation tiles on, rows_matmul_lds_kernel stages
+// the activations through LDS instead (see there).
 //
 // An operand tile spans 16 weight rows, so from a row-major w_t each load
 // instruction fetches 64 bytes from each of 16 rows K * 2 bytes apart.  The
@@ -158,20 +159,169 @@ void rows_matmul_kernel(const uint16_t* __restrict__ a,
   }
 }
 
+// Two or more activation tiles: the activations are staged through LDS.
+// Read as MFMA operands straight from a row-major matrix, every load
+// instruction takes a 64-byte slice of 16 rows 2K bytes apart -- half of 16
+// cache lines -- and a probe streaming the same 80 x 4096 block that way
+// per workgroup ran 2.7 times slower than in 1 KB contiguous pieces.  So
+// four loader waves copy a 256-wide K chunk of every row into LDS with
+// memory-to-LDS loads (each instruction two rows' 512 contiguous bytes),
+// double-buffered, and four compute waves read their activation operands
+// from there while their weights stream into registers, eight steps per
+// wave in flight.  Keeping the two streams in different waves keeps the
+// activations' L2 hits from queueing behind the weights' HBM reads (a
+// wave's loads complete in order).  The chunk's 16-byte pieces are stored
+// XOR-swizzled by row (piece q of row r at position q ^ (r % 16)), so the
+// 16 rows of an operand read hit 16 different bank groups.  Each compute
+// wave still takes steps wave, wave + 4, ... in order and the waves' sums
+// are added in wave order: the same sums as rows_matmul_kernel, bit for bit.
+typedef __attribute__((address_space(3))) void* lds_ptr_t;
+constexpr int kChunkK = 256;               // K values per staged chunk (512 bytes a row)
+constexpr int kChunkSteps = kChunkK / 32;  // 8 MFMA steps, two per compute wave
+// Weight chunks requested ahead (two fragments each per compute wave), and
+// staged activation chunks; deeper settings (8 weight chunks, 3-4 staged
+// chunks where LDS holds them) measured the same.
+constexpr int kWChunksAhead = 4;
+constexpr int kStages = 2;
+
+template <int MT, class OutT, bool PACKED>
+__global__ __launch_bounds__(128 * kWaves) void rows_matmul_lds_kernel(const uint16_t* __restrict__ a,
+                                                                       const uint16_t* __restrict__ w_t,
+                                                                       OutT* __restrict__ out, int M, int K,
+                                                                       int N) {
+  constexpr int kRows = 16 * MT;
+  constexpr int kBuf = kRows * kChunkK * 2;   // bytes of one staged chunk
+  constexpr int kInstr = kRows / 2 / kWaves;  // memory-to-LDS loads per loader wave per chunk
+  constexpr int WA = kWChunksAhead, NB = kStages;
+  constexpr int kWAhead = 2 * WA;             // weight fragments in flight per compute wave
+  __shared__ __attribute__((aligned(1024))) char abuf[NB * kBuf];
+  __shared__ f32x4_t part[kWaves - 1][MT][64];
+
+  const int wid = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6), lane = threadIdx.x & 63;
+  const bool loader = wid >= kWaves;
+  const int wave = wid % kWaves;  // compute wave, or loader index
+  const int c = lane & 15, g = lane >> 4;
+  const int n0 = blockIdx.x * 16;
+  const int w_rows = min(16, N - n0);
+  const int k_steps = (K + 31) / 32;
+  const int chunks = (K + kChunkK - 1) / kChunkK;
+  const __amdgpu_buffer_rsrc_t rw = PACKED
+      ? __builtin_amdgcn_make_buffer_rsrc(const_cast<uint16_t*>(w_t) + (size_t)blockIdx.x * k_steps * 512,
+                                          (short)0, k_steps * 1024, kDesc3)
+      : __builtin_amdgcn_make_buffer_rsrc(const_cast<uint16_t*>(w_t) + (size_t)n0 * K, (short)0,
+                                          w_rows * K * 2, kDesc3);
+  // rows past M and columns past K read as zeros
+  const __amdgpu_buffer_rsrc_t ra = __builtin_amdgcn_make_buffer_rsrc(const_cast<uint16_t*>(a), (short)0,
+                                                                      M * K * 2, kDesc3);
+  // weight operand of step st for this lane (zeros past K)
+  auto wload = [&](int st) {
+    const int kk = 32 * st + 8 * g;
+    const int off = kk < K ? (PACKED ? st * 1024 + 16 * lane : c * K * 2 + kk * 2) : kOutOfRange;
+    return load16<kStream>(rw, off);
+  };
+  // a loader wave's part of chunk ch into buffer b: instruction i covers
+  // rows 2i and 2i + 1, lane l piece (l % 32) ^ (r % 16) of row r = 2i + l / 32
+  auto stage = [&](int ch, int b) {
+#pragma unroll
+    for (int j = 0; j < kInstr; ++j) {
+      const int i = wave + kWaves * j;
+      const int r = 2 * i + (lane >> 5);
+      const int kk = ch * kChunkK + 8 * ((lane & 31) ^ (r & 15));
+      const int off = kk < K ? (r * K + kk) * 2 : kOutOfRange;
+      __builtin_amdgcn_raw_ptr_buffer_load_lds(ra, (lds_ptr_t)(abuf + b * kBuf + i * 1024), 16, off, 0, 0, 0);
+    }
+  };
+
+  f32x4_t acc[MT];
+#pragma unroll
+  for (int t = 0; t < MT; ++t) acc[t] = f32x4_t{0.f, 0.f, 0.f, 0.f};
+  u32x4_t wf[kWAhead];  // slot 2 (ch % WA) + h: step ch * 8 + wave + 4 h
+
+  if (loader) {
+#pragma unroll
+    for (int b = 0; b < NB; ++b)
+      if (b < chunks) stage(b, b);
+  } else {
+#pragma unroll
+    for (int i = 0; i < kWAhead; ++i) wf[i] = wload((i / 2) * kChunkSteps + wave + kWaves * (i % 2));
+  }
+
+  for (int ch0 = 0; ch0 < chunks; ch0 += kWAhead / 2) {
+#pragma unroll
+    for (int u = 0; u < kWAhead / 2; ++u) {
+      const int ch = ch0 + u;
+      if (ch < chunks) {
+        // Chunk ch staged: each loader wave waits for its own loads of it
+        // (only the next chunk's may still be in flight), then all meet.
+        if (loader) {
+          if (ch + 1 < chunks)  // the next chunk's loads may stay in flight
+            asm volatile("s_waitcnt vmcnt(%0)" ::"n"(kInstr) : "memory");
+          else
+            asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
+        }
+        asm volatile("s_barrier" ::: "memory");
+        const int bi = ch & 1;
+        if (!loader) {
+          const char* buf = abuf + bi * kBuf;
+#pragma unroll
+          for (int h = 0; h < 2; ++h) {
+            const int sq = 4 * (wave + kWaves * h) + g;  // piece of this lane's operand
+#pragma unroll
+            for (int t = 0; t < MT; ++t) {
+              const u32x4_t av = *(const u32x4_t*)(buf + (16 * t + c) * 512 + 16 * (sq ^ c));
+              acc[t] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8_t, wf[2 * u + h]),
+                                                              __builtin_bit_cast(bf16x8_t, av), acc[t], 0, 0, 0);
+            }
+          }
+#pragma unroll
+          for (int h = 0; h < 2; ++h) wf[2 * u + h] = wload((ch + WA) * kChunkSteps + wave + kWaves * h);
+        }
+        asm volatile("s_barrier" ::: "memory");  // every wave is done with buffer bi
+        if (loader && ch + NB < chunks) stage(ch + NB, bi);
+      }
+    }
+  }
+
+  // Sum the four compute waves' partial products through LDS; wave 0 writes.
+  if (!loader && wave > 0) {
+#pragma unroll
+    for (int t = 0; t < MT; ++t) part[wave - 1][t][lane] = acc[t];
+  }
+  __syncthreads();
+  if (loader || wave != 0) return;
+#pragma unroll
+  for (int t = 0; t < MT; ++t) {
+#pragma unroll
+    for (int w = 0; w < kWaves - 1; ++w) acc[t] += part[w][t][lane];
+    const int m = 16 * t + c;
+    if (m < M) {
+#pragma unroll
+      for (int r = 0; r < 4; ++r) {
+        const int n = n0 + 4 * g + r;
+        if (n < N) store_out(out + (size_t)m * N + n, acc[t][r]);
+      }
+    }
+  }
+}
+
 template <class OutT, bool PACKED>
 hipError_t launch_rows(const uint16_t* a, const uint16_t* w_t, OutT* out, int M, int K, int N,
                        hipStream_t stream) {
-  const dim3 grid((N + 15) / 16), block(64 * kWaves);
+  const dim3 grid((N + 15) / 16), block(64 * kWaves), block_lds(128 * kWaves);
   const int mt = (M + 15) / 16;
+  // One or two activation tiles: operands straight from memory (the LDS
+  // staging measured slower there: 13.3 against 10.2 us at 17 rows, equal
+  // at 32); more: activations staged through LDS (80 rows: 16.3 against
+  // 25.6 us).
   switch (mt) {
     case 1: hipLaunchKernelGGL((rows_matmul_kernel<1, OutT, PACKED>), grid, block, 0, stream, a, w_t, out, M, K, N); break;
     case 2: hipLaunchKernelGGL((rows_matmul_kernel<2, OutT, PACKED>), grid, block, 0, stream, a, w_t, out, M, K, N); break;
-    case 3: hipLaunchKernelGGL((rows_matmul_kernel<3, OutT, PACKED>), grid, block, 0, stream, a, w_t, out, M, K, N); break;
-    case 4: hipLaunchKernelGGL((rows_matmul_kernel<4, OutT, PACKED>), grid, block, 0, stream, a, w_t, out, M, K, N); break;
-    case 5: hipLaunchKernelGGL((rows_matmul_kernel<5, OutT, PACKED>), grid, block, 0, stream, a, w_t, out, M, K, N); break;
-    case 6: hipLaunchKernelGGL((rows_matmul_kernel<6, OutT, PACKED>), grid, block, 0, stream, a, w_t, out, M, K, N); break;
-    case 7: hipLaunchKernelGGL((rows_matmul_kernel<7, OutT, PACKED>), grid, block, 0, stream, a, w_t, out, M, K, N); break;
-    default: hipLaunchKernelGGL((rows_matmul_kernel<8, OutT, PACKED>), grid, block, 0, stream, a, w_t, out, M, K, N); break;
+    case 3: hipLaunchKernelGGL((rows_matmul_lds_kernel<3, OutT, PACKED>), grid, block_lds, 0, stream, a, w_t, out, M, K, N); break;
+    case 4: hipLaunchKernelGGL((rows_matmul_lds_kernel<4, OutT, PACKED>), grid, block_lds, 0, stream, a, w_t, out, M, K, N); break;
+    case 5: hipLaunchKernelGGL((rows_matmul_lds_kernel<5, OutT, PACKED>), grid, block_lds, 0, stream, a, w_t, out, M, K, N); break;
+    case 6: hipLaunchKernelGGL((rows_matmul_lds_kernel<6, OutT, PACKED>), grid, block_lds, 0, stream, a, w_t, out, M, K, N); break;
+    case 7: hipLaunchKernelGGL((rows_matmul_lds_kernel<7, OutT, PACKED>), grid, block_lds, 0, stream, a, w_t, out, M, K, N); break;
+    default: hipLaunchKernelGGL((rows_matmul_lds_kernel<8, OutT, PACKED>), grid, block_lds, 0, stream, a, w_t, out, M, K, N); break;
   }
   return hipGetLastError();
 }
