@@ -197,3 +197,33 @@ def test_rows_matmul_one_pass_matches_row_blocks(M):
         torch.cuda.synchronize()
         assert torch.equal(one.view(view), parts.view(view))
         assert torch.equal(onep.view(view), one.view(view))
+
+
+@pytest.mark.parametrize("M,K,N", [(33, 264, 17), (48, 8, 40), (100, 520, 33), (128, 4104, 64)])
+def test_rows_matmul_staged_matches_direct(M, K, N):
+    """From 33 rows the activations are staged through LDS in 256-wide K
+    chunks (swizzled pieces, a partial last chunk, rows past M as zeros);
+    each output row must still be the direct kernel's dot products in the
+    same order: one launch equals, bit for bit, the rows taken 32 at a time
+    (the direct kernel), and stays within the oracle's bound."""
+    require_gpu()
+    say("rows_matmul staged vs direct", dict(M=M, K=K, N=N))
+    a = _bf16((M, K), 51 + M).cuda()
+    w_t = _bf16((N, K), 52 + N, 1.0 / np.sqrt(K)).cuda()
+    packed = glide.pack_rows_weights(w_t)
+    for out_dtype in (torch.bfloat16, torch.float32):
+        view = torch.int16 if out_dtype == torch.bfloat16 else torch.int32
+        for weights, call in ((w_t, glide.glide_rows_matmul), (packed, glide.glide_rows_matmul_packed)):
+            one = torch.full((M, N), float("nan"), dtype=out_dtype, device="cuda")
+            rows = torch.full((M, N), float("nan"), dtype=out_dtype, device="cuda")
+            call(a, weights, one)
+            for m0 in range(0, M, 32):
+                m1 = min(M, m0 + 32)
+                call(a[m0:m1].contiguous(), weights, rows[m0:m1])
+            torch.cuda.synchronize()
+            assert torch.equal(one.view(view), rows.view(view))
+    want = OX.rows_matmul(to64(a.cpu()), to64(w_t.cpu()))
+    out = torch.full((M, N), float("nan"), dtype=torch.float32, device="cuda")
+    glide.glide_rows_matmul(a, w_t, out)
+    torch.cuda.synchronize()
+    assert float(np.abs(to64(out) - want).max()) <= F32_OUT_TOL
