@@ -1109,6 +1109,11 @@ __global__ __launch_bounds__(kThreads) void tree_attn_combine(AttnArgs args) {
     ml[u] = args.part_ml[base + (size_t)sp * N];
     ov[u] = *(const float2*)(args.part_o + (base + (size_t)sp * N) * kD + 2 * lane);
   }
+  // Pin the batch's loads above the early return below: the compiler
+  // otherwise sinks them past it, and the partials are only requested once
+  // the length has arrived (two round trips instead of one).
+#pragma unroll
+  for (int u = 0; u < kBatch; ++u) asm volatile("" : "+v"(ml[u].x), "+v"(ml[u].y), "+v"(ov[u].x), "+v"(ov[u].y));
   const int Lb = min(max(raw_len, 0), tree ? Lcap - N : Lcap);
   const int T = Lb + (tree ? N : 0);
   const int nsplit = max(1, (T + args.chunk - 1) / args.chunk);
