@@ -13,8 +13,8 @@
 // same operand shapes as the attention kernel's K * Q^T.  Loads go through
 // range-checked buffer descriptors (weight rows past N and activation rows
 // past M read as zeros), five to eight steps in flight per wave in
-// registers.  From three activation tiles on, rows_matmul_lds_kernel stages
-// the activations through LDS instead (see there).
+// registers.  From 21 activation rows on, rows_matmul_lds_kernel stages the
+// activations through LDS instead (see there).
 //
 // An operand tile spans 16 weight rows, so from a row-major w_t each load
 // instruction fetches 64 bytes from each of 16 rows K * 2 bytes apart.  The
@@ -164,7 +164,7 @@ void rows_matmul_kernel(const uint16_t* __restrict__ a,
   }
 }
 
-// Two or more activation tiles: the activations are staged through LDS.
+// From 21 activation rows: the activations are staged through LDS.
 // Read as MFMA operands straight from a row-major matrix, every load
 // instruction takes a 64-byte slice of 16 rows 2K bytes apart -- half of 16
 // cache lines -- and a probe streaming the same 80 x 4096 block that way
@@ -327,13 +327,18 @@ hipError_t launch_rows(const uint16_t* a, const uint16_t* w_t, OutT* out, int M,
                        hipStream_t stream) {
   const dim3 grid((N + 15) / 16), block(64 * kWaves), block_lds(128 * kWaves);
   const int mt = (M + 15) / 16;
-  // One or two activation tiles: operands straight from memory (the LDS
-  // staging measured slower there: 13.3 against 10.2 us at 17 rows, equal
-  // at 32); more: activations staged through LDS (80 rows: 16.3 against
-  // 25.6 us).
+  // Up to 20 rows the operands come straight from memory; from 21 rows the
+  // activations are staged through LDS (K = N = 4096, packed weights: 17
+  // rows 9.6 against 10.3 us staged, 24 rows 11.3 against 10.3, 32 rows
+  // 13.1 against 10.4, 80 rows 25.6 against 14.4).  Both give the same sums.
   switch (mt) {
     case 1: hipLaunchKernelGGL((rows_matmul_kernel<1, OutT, PACKED>), grid, block, 0, stream, a, w_t, out, M, K, N); break;
-    case 2: hipLaunchKernelGGL((rows_matmul_kernel<2, OutT, PACKED>), grid, block, 0, stream, a, w_t, out, M, K, N); break;
+    case 2:
+      if (M > 20)
+        hipLaunchKernelGGL((rows_matmul_lds_kernel<2, OutT, PACKED>), grid, block_lds, 0, stream, a, w_t, out, M, K, N);
+      else
+        hipLaunchKernelGGL((rows_matmul_kernel<2, OutT, PACKED>), grid, block, 0, stream, a, w_t, out, M, K, N);
+      break;
     case 3: hipLaunchKernelGGL((rows_matmul_lds_kernel<3, OutT, PACKED>), grid, block_lds, 0, stream, a, w_t, out, M, K, N); break;
     case 4: hipLaunchKernelGGL((rows_matmul_lds_kernel<4, OutT, PACKED>), grid, block_lds, 0, stream, a, w_t, out, M, K, N); break;
     case 5: hipLaunchKernelGGL((rows_matmul_lds_kernel<5, OutT, PACKED>), grid, block_lds, 0, stream, a, w_t, out, M, K, N); break;

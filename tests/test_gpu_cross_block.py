@@ -199,12 +199,13 @@ def test_rows_matmul_one_pass_matches_row_blocks(M):
         assert torch.equal(onep.view(view), one.view(view))
 
 
-@pytest.mark.parametrize("M,K,N", [(33, 264, 17), (48, 8, 40), (100, 520, 33), (128, 4104, 64)])
+@pytest.mark.parametrize("M,K,N", [(21, 520, 40), (32, 4104, 17), (33, 264, 17), (48, 8, 40),
+                                   (100, 520, 33), (128, 4104, 64)])
 def test_rows_matmul_staged_matches_direct(M, K, N):
-    """From 33 rows the activations are staged through LDS in 256-wide K
+    """From 21 rows the activations are staged through LDS in 256-wide K
     chunks (swizzled pieces, a partial last chunk, rows past M as zeros);
     each output row must still be the direct kernel's dot products in the
-    same order: one launch equals, bit for bit, the rows taken 32 at a time
+    same order: one launch equals, bit for bit, the rows taken 16 at a time
     (the direct kernel), and stays within the oracle's bound."""
     require_gpu()
     say("rows_matmul staged vs direct", dict(M=M, K=K, N=N))
@@ -217,8 +218,8 @@ def test_rows_matmul_staged_matches_direct(M, K, N):
             one = torch.full((M, N), float("nan"), dtype=out_dtype, device="cuda")
             rows = torch.full((M, N), float("nan"), dtype=out_dtype, device="cuda")
             call(a, weights, one)
-            for m0 in range(0, M, 32):
-                m1 = min(M, m0 + 32)
+            for m0 in range(0, M, 16):
+                m1 = min(M, m0 + 16)
                 call(a[m0:m1].contiguous(), weights, rows[m0:m1])
             torch.cuda.synchronize()
             assert torch.equal(one.view(view), rows.view(view))
